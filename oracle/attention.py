@@ -37,15 +37,17 @@ def attend_rows(q, k, v, rows, cu_seqlens, scale=None) -> np.ndarray:
     if scale is None:
         scale = 1.0 / np.sqrt(d)
     cu = np.asarray(cu_seqlens, dtype=np.int64)
+    group = [np.array([h for h in range(Hq) if (h * Hkv) // Hq == g]) for g in range(Hkv)]
     out = np.empty((len(rows), Hq, d), dtype=np.float64)
     for n, t in enumerate(np.asarray(rows, dtype=np.int64)):
         b = int(np.searchsorted(cu, t, side="right") - 1)
         lo = int(cu[b])
-        for h in range(Hq):
-            g = (h * Hkv) // Hq
-            s = (k[g, lo:t + 1, :] @ q[t, h, :]) * scale
-            p = np.exp(s - s.max())
-            out[n, h, :] = (p @ v[g, lo:t + 1, :]) / p.sum()
+        for g in range(Hkv):
+            hs = group[g]
+            # one score row per query head of the group, over keys lo..t
+            s = (q[t, hs, :] @ k[g, lo:t + 1, :].T) * scale
+            p = np.exp(s - s.max(axis=1, keepdims=True))
+            out[n, hs, :] = (p @ v[g, lo:t + 1, :]) / p.sum(axis=1, keepdims=True)
     return out
 
 

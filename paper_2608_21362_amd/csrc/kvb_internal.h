@@ -1,0 +1,59 @@
+// Internal declarations shared by the HIP translation units of libkvb.
+// Launchers validate nothing: the C entry points in kvb_api.cpp have already
+// checked every host-visible argument.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kvb.h"
+
+namespace kvb {
+
+// ---- population ---------------------------------------------------------
+hipError_t launch_rope_rows(int head_dim, int64_t n_outer, int64_t n_rows, int64_t n_inner,
+                            const float* x, const int32_t* row_pos, const int32_t* outer_pos,
+                            const float* tcos, const float* tsin, int32_t table_len,
+                            kvb_dtype out_dtype, void* out, hipStream_t s);
+
+hipError_t launch_kivi_quantize(const kvb_pool_layout& p, int32_t n_pool, int32_t first_layer,
+                                int32_t n_in, kvb_dtype in_dtype, const void* k_in,
+                                const void* v_in, uint8_t* k_codes, float* k_scale, float* k_zero,
+                                uint8_t* v_codes, float* v_scale, float* v_zero, hipStream_t s);
+
+// ---- hot path -------------------------------------------------------------
+hipError_t launch_stitch(const kvb_pool_layout& p, int32_t n_pool, const uint8_t* k_codes,
+                         const float* k_scale, const float* k_zero, const uint8_t* v_codes,
+                         const float* v_scale, const float* v_zero, const kvb_chunk* chunks,
+                         int32_t n_chunks, const float* rope_cos, const float* rope_sin,
+                         int64_t t_total, kvb_dtype out_dtype, void* k_cache, void* v_cache,
+                         hipStream_t s);
+
+hipError_t launch_deviation(int n_layers, int n_kv_heads, int head_dim, int64_t t_total,
+                            const uint16_t* k_cache, const uint16_t* k_fresh,
+                            const uint16_t* v_cache, const uint16_t* v_fresh, int per_layer,
+                            float* delta, hipStream_t s);
+
+size_t select_workspace_bytes(int32_t n_sets, int64_t t_total, int32_t n_seqs);
+hipError_t launch_select(int32_t n_sets, int64_t t_total, const int32_t* cu_seqlens,
+                         int32_t n_seqs, const float* delta, const uint8_t* row_flags,
+                         const int32_t* k_per_seq, int32_t* rows, int32_t* cu_rows,
+                         void* workspace, hipStream_t s);
+
+struct AttnPlan {
+  int rows_per_tile;   // selected rows per workgroup tile
+  int tile_slots;      // tile slots per (layer, kv head)
+  int split_len;       // keys per split (multiple of the key block)
+  int n_split_max;     // splits per tile slot
+  size_t workspace;    // bytes of split partials
+};
+bool attn_plan(int n_layers, int n_q_heads, int n_kv_heads, int head_dim, int64_t t_total,
+               int n_seqs, int max_seq_len, int max_rows, AttnPlan* plan);
+hipError_t launch_sparse_attn(const AttnPlan& plan, int n_layers, int n_q_heads, int n_kv_heads,
+                              int head_dim, int64_t t_total, const int32_t* cu_seqlens,
+                              int n_seqs, const int32_t* rows, const int32_t* cu_rows,
+                              int rows_per_layer, int max_rows, const uint16_t* q,
+                              const uint16_t* k_fresh, const uint16_t* v_fresh,
+                              uint16_t* k_cache, uint16_t* v_cache, float softmax_scale,
+                              kvb_dtype out_dtype, void* out, void* workspace, hipStream_t s);
+
+}  // namespace kvb

@@ -1,0 +1,184 @@
+// Stitch: dequantise cached KIVI chunks and rotate their keys from the cached
+// position to the new one (Sec. 4.3 assembly, Sec. 3.2 R^Delta, Sec. 4.5).
+//
+// One workgroup per (chunk, layer, kv head): 128 tokens x d channels of K and
+// of V.  HBM-bound: per workgroup it reads the K and V code blocks (C*d*b/8
+// bytes each) and their float statistics, and writes 2*C*d output elements.
+//
+// Key jobs: one thread takes 4 consecutive tokens (one statistic group,
+// Gk % 4 == 0) and 8 channel pairs (j, j + d/2); statistics and the chunk's
+// rotation row are loaded and widened to double once per job.  Value jobs:
+// one thread takes one token and 16 consecutive channels (one statistic group,
+// Gv % 16 == 0).
+//
+// Arithmetic is double with contraction off: x = fma(code, scale, zero) is
+// exact in the product (8-bit code times 24-bit scale), so it equals the
+// product-then-sum form; the rotation is mul, mul, sub / add.  The double is
+// rounded to float, and for bfloat16 output the float is rounded again.
+#include "kvb_device.h"
+#include "kvb_internal.h"
+
+namespace kvb {
+namespace {
+
+constexpr int kC = 128;
+
+template <int BITS, int D, bool BF16>
+__global__ void __launch_bounds__(256)
+stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
+              const uint8_t* __restrict__ k_codes, const float* __restrict__ k_scale,
+              const float* __restrict__ k_zero, const uint8_t* __restrict__ v_codes,
+              const float* __restrict__ v_scale, const float* __restrict__ v_zero,
+              const kvb_chunk* __restrict__ chunks, const float* __restrict__ rope_cos,
+              const float* __restrict__ rope_sin, int64_t t_total, void* __restrict__ k_out,
+              void* __restrict__ v_out) {
+  constexpr int H = D / 2;
+  constexpr int CB = D * BITS / 8;       // code bytes per token row
+  constexpr int TPT = H / 8;             // key threads per token quad
+  constexpr int KJOBS = (kC / 4) * TPT;  // 256 (d=128) or 128 (d=64)
+  constexpr int VJOBS = kC * (D / 16);
+  const int c = blockIdx.x;
+  const int lh = blockIdx.y;
+  const int l = lh / Hkv, h = lh % Hkv;
+  const kvb_chunk ch = chunks[c];
+  if (ch.pool_idx < 0 || ch.pool_idx >= n_pool || ch.dst_row < 0 ||
+      (int64_t)ch.dst_row + kC > t_total)
+    return;
+  const int64_t slab = ((int64_t)ch.pool_idx * L + l) * Hkv + h;  // (p, l, h)
+  const int64_t out_row0 = ((int64_t)l * Hkv + h) * t_total + ch.dst_row;
+  const int ngk = kC / Gk, ngv = D / Gv;
+
+  for (int job = threadIdx.x; job < KJOBS + VJOBS; job += blockDim.x) {
+    if (job < KJOBS) {
+      // ---- keys: tokens 4q..4q+3, channel pairs [8cg, 8cg + 8)
+      const int q = job / TPT, cg = job % TPT;
+      const int u0 = 4 * q, j0 = 8 * cg;
+      const int g = u0 / Gk;
+      const float* sc = k_scale + (slab * ngk + g) * D;
+      const float* zr = k_zero + (slab * ngk + g) * D;
+      double s_lo[8], s_hi[8], z_lo[8], z_hi[8], cs[8], sn[8];
+#pragma unroll
+      for (int k = 0; k < 8; k += 4) {
+        const float4 a = *reinterpret_cast<const float4*>(sc + j0 + k);
+        const float4 b = *reinterpret_cast<const float4*>(sc + H + j0 + k);
+        const float4 e = *reinterpret_cast<const float4*>(zr + j0 + k);
+        const float4 f = *reinterpret_cast<const float4*>(zr + H + j0 + k);
+        const float4 cc = *reinterpret_cast<const float4*>(rope_cos + (int64_t)c * H + j0 + k);
+        const float4 ss = *reinterpret_cast<const float4*>(rope_sin + (int64_t)c * H + j0 + k);
+        s_lo[k] = a.x; s_lo[k + 1] = a.y; s_lo[k + 2] = a.z; s_lo[k + 3] = a.w;
+        s_hi[k] = b.x; s_hi[k + 1] = b.y; s_hi[k + 2] = b.z; s_hi[k + 3] = b.w;
+        z_lo[k] = e.x; z_lo[k + 1] = e.y; z_lo[k + 2] = e.z; z_lo[k + 3] = e.w;
+        z_hi[k] = f.x; z_hi[k + 1] = f.y; z_hi[k + 2] = f.z; z_hi[k + 3] = f.w;
+        cs[k] = cc.x; cs[k + 1] = cc.y; cs[k + 2] = cc.z; cs[k + 3] = cc.w;
+        sn[k] = ss.x; sn[k + 1] = ss.y; sn[k + 2] = ss.z; sn[k + 3] = ss.w;
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int u = u0 + i;
+        const uint8_t* row = k_codes + (slab * kC + u) * CB;
+        uint32_t wl[2], wh[2];
+        if constexpr (BITS == 8) {
+          const uint2 a = *reinterpret_cast<const uint2*>(row + j0);
+          const uint2 b = *reinterpret_cast<const uint2*>(row + H + j0);
+          wl[0] = a.x; wl[1] = a.y; wh[0] = b.x; wh[1] = b.y;
+        } else {
+          wl[0] = *reinterpret_cast<const uint32_t*>(row + j0 / 2);
+          wh[0] = *reinterpret_cast<const uint32_t*>(row + (H + j0) / 2);
+          wl[1] = wh[1] = 0;
+        }
+        float ylo[8], yhi[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const double xl = __builtin_fma((double)code_at<BITS>(wl, k), s_lo[k], z_lo[k]);
+          const double xh = __builtin_fma((double)code_at<BITS>(wh, k), s_hi[k], z_hi[k]);
+          const double a = xl * cs[k];
+          const double b = xh * sn[k];
+          const double e = xh * cs[k];
+          const double f = xl * sn[k];
+          ylo[k] = (float)(a - b);
+          yhi[k] = (float)(e + f);
+        }
+        const int64_t o = (out_row0 + u) * D;
+        if constexpr (BF16) {
+          uint16_t* ko = reinterpret_cast<uint16_t*>(k_out) + o;
+          uint4 A, B;
+          A.x = pack_bf16x2(ylo[0], ylo[1]); A.y = pack_bf16x2(ylo[2], ylo[3]);
+          A.z = pack_bf16x2(ylo[4], ylo[5]); A.w = pack_bf16x2(ylo[6], ylo[7]);
+          B.x = pack_bf16x2(yhi[0], yhi[1]); B.y = pack_bf16x2(yhi[2], yhi[3]);
+          B.z = pack_bf16x2(yhi[4], yhi[5]); B.w = pack_bf16x2(yhi[6], yhi[7]);
+          *reinterpret_cast<uint4*>(ko + j0) = A;
+          *reinterpret_cast<uint4*>(ko + H + j0) = B;
+        } else {
+          float* ko = reinterpret_cast<float*>(k_out) + o;
+          *reinterpret_cast<float4*>(ko + j0) = make_float4(ylo[0], ylo[1], ylo[2], ylo[3]);
+          *reinterpret_cast<float4*>(ko + j0 + 4) = make_float4(ylo[4], ylo[5], ylo[6], ylo[7]);
+          *reinterpret_cast<float4*>(ko + H + j0) = make_float4(yhi[0], yhi[1], yhi[2], yhi[3]);
+          *reinterpret_cast<float4*>(ko + H + j0 + 4) = make_float4(yhi[4], yhi[5], yhi[6], yhi[7]);
+        }
+      }
+    } else {
+      // ---- values: token u, channels [16vg, 16vg + 16)
+      const int vj = job - KJOBS;
+      const int u = vj / (D / 16), vg = vj % (D / 16);
+      const int j0 = vg * 16;
+      const int64_t srow = slab * kC + u;
+      const double sc = v_scale[srow * ngv + j0 / Gv];
+      const double zr = v_zero[srow * ngv + j0 / Gv];
+      const uint8_t* row = v_codes + srow * CB;
+      uint32_t w[4];
+      if constexpr (BITS == 8) {
+        const uint4 a = *reinterpret_cast<const uint4*>(row + j0);
+        w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
+      } else {
+        const uint2 a = *reinterpret_cast<const uint2*>(row + j0 / 2);
+        w[0] = a.x; w[1] = a.y; w[2] = w[3] = 0;
+      }
+      float y[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) y[k] = (float)__builtin_fma((double)code_at<BITS>(w, k), sc, zr);
+      const int64_t o = (out_row0 + u) * D + j0;
+      if constexpr (BF16) {
+        uint16_t* vo = reinterpret_cast<uint16_t*>(v_out) + o;
+        uint4 A, B;
+        A.x = pack_bf16x2(y[0], y[1]);   A.y = pack_bf16x2(y[2], y[3]);
+        A.z = pack_bf16x2(y[4], y[5]);   A.w = pack_bf16x2(y[6], y[7]);
+        B.x = pack_bf16x2(y[8], y[9]);   B.y = pack_bf16x2(y[10], y[11]);
+        B.z = pack_bf16x2(y[12], y[13]); B.w = pack_bf16x2(y[14], y[15]);
+        *reinterpret_cast<uint4*>(vo) = A;
+        *reinterpret_cast<uint4*>(vo + 8) = B;
+      } else {
+        float* vo = reinterpret_cast<float*>(v_out) + o;
+#pragma unroll
+        for (int k = 0; k < 16; k += 4)
+          *reinterpret_cast<float4*>(vo + k) = make_float4(y[k], y[k + 1], y[k + 2], y[k + 3]);
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_stitch(const kvb_pool_layout& p, int32_t n_pool, const uint8_t* k_codes,
+                         const float* k_scale, const float* k_zero, const uint8_t* v_codes,
+                         const float* v_scale, const float* v_zero, const kvb_chunk* chunks,
+                         int32_t n_chunks, const float* rope_cos, const float* rope_sin,
+                         int64_t t_total, kvb_dtype out_dtype, void* k_cache, void* v_cache,
+                         hipStream_t s) {
+  const dim3 grid(n_chunks, p.n_layers * p.n_kv_heads), block(256);
+  const bool bf = out_dtype == KVB_BF16;
+#define KVB_STITCH(B, D, F)                                                                       \
+  hipLaunchKernelGGL((stitch_kernel<B, D, F>), grid, block, 0, s, p.n_layers, p.n_kv_heads,      \
+                     p.k_group, p.v_group, n_pool, k_codes, k_scale, k_zero, v_codes, v_scale,   \
+                     v_zero, chunks, rope_cos, rope_sin, t_total, k_cache, v_cache)
+  if (p.bits == 8) {
+    if (p.head_dim == 128) { if (bf) KVB_STITCH(8, 128, true); else KVB_STITCH(8, 128, false); }
+    else { if (bf) KVB_STITCH(8, 64, true); else KVB_STITCH(8, 64, false); }
+  } else {
+    if (p.head_dim == 128) { if (bf) KVB_STITCH(4, 128, true); else KVB_STITCH(4, 128, false); }
+    else { if (bf) KVB_STITCH(4, 64, true); else KVB_STITCH(4, 64, false); }
+  }
+#undef KVB_STITCH
+  return hipGetLastError();
+}
+
+}  // namespace kvb

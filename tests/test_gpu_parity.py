@@ -1,0 +1,293 @@
+"""GPU parity: the HIP path against the CPU oracle on the same seeded draws.
+
+Each side builds its own inputs from ``kvb_workload``'s raw draws (the oracle
+with ``oracle.populate``, the library with its population kernels) and runs
+its own path.  Acceptance, per step:
+
+* population and stitch (float64 arithmetic on both sides, one rounding to
+  float32, one more to bfloat16): bit-exact;
+* deviation: within one float32 ulp of the oracle's float64 value rounded to
+  float32 (float64 sums in different orders);
+* selection: bit-exact on the same deviations (stage-isolated, ties
+  included); end to end bit-exact unless the oracle's k-th / (k+1)-th margin
+  is within 1e-4, in which case every differing row must lie within 1e-4 of
+  the k-th deviation;
+* patch: selected cache rows equal the fresh rows bitwise, all others are
+  unchanged;
+* attention: |o - o_ref| <= 2e-2 + 1e-2 |o_ref| elementwise against the
+  float64 oracle; rows outside the selection stay untouched.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import kvb_workload as kw
+from oracle import attention as oatt
+from oracle import deviation as odev
+from oracle import numerics, populate as opop, selection as osel, stitch as ostitch
+
+pytestmark = pytest.mark.gpu
+
+ATOL, RTOL = 2e-2, 1e-2
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _np16(t):
+    return t.detach().cpu().numpy().view(np.uint16)
+
+
+# Small cases: several tiles of every kernel, a ragged tail, both code widths,
+# both head sizes, sinks, seams, several prompts and several layers.
+SMALL = {
+    "tiny": kw.WORKLOADS["tiny"],
+    "qwen_1l": kw.WORKLOADS["qwen_1l"],
+    "int4_2l": kw.scaled(kw.WORKLOADS["qwen_36l_8k"], n_layers=2, chunks_per_prompt=9),
+    "sinks_seams_2l": kw.scaled(kw.WORKLOADS["long_32k"], n_layers=2, chunks_per_prompt=7),
+    "batched_small": kw.scaled(kw.WORKLOADS["batched_mixed"], n_prompts=3, chunks_per_prompt=5),
+    "all_layer_delta": kw.scaled(kw.WORKLOADS["qwen_36l_8k"], n_layers=3, chunks_per_prompt=4,
+                                 per_layer=False, seam_left=16, seam_right=0),
+}
+
+
+class Case:
+    """Both sides of one workload, built once per module."""
+
+    def __init__(self, w, layers=None):
+        from paper_2608_21362_amd import pipeline
+
+        _need_gpu()
+        self.w = w
+        self.s = kw.structure(w)
+        self.layers = list(range(w.n_layers)) if layers is None else layers
+        _say(f"[case] {w.name} L={w.n_layers} T={w.t_total} layers={self.layers}")
+        self.dev = pipeline.populate(w, self.s)
+        self.ref = opop.populate(w, self.s, layers=self.layers)
+        self.pb = pipeline.buffers(self.dev)
+        pipeline.run_path(self.dev, self.pb)
+        torch.cuda.synchronize()
+        self.ck = opop.SENTINEL_BF16
+        # oracle path on the same layers
+        ck, cv = self.ref.cache_k.copy(), self.ref.cache_v.copy()
+        ostitch.stitch_into(ck, cv, self.ref.pool, self.ref.chunks, self.ref.cos, self.ref.sin, "bf16")
+        self.ref_ck, self.ref_cv = ck, cv
+        if w.per_layer:
+            self.ref_delta = odev.deviation(ck, self.ref.k_fresh, per_layer=True)
+        else:
+            self.ref_delta = odev.deviation(ck, self.ref.k_fresh, per_layer=False)
+        cand = self.s.hit_row
+        self.forced = osel.forced_rows(self.s.cu_seqlens, self.s.hit_row, self.s.chunk_starts,
+                                       w.seam_left, w.seam_right)
+        self.kseq = osel.k_per_prompt(self.s.cu_seqlens, cand, w.rho_num, w.rho_den)
+
+    def gpu_layer(self, i):
+        return self.layers[i]
+
+
+_CASES = {}
+
+
+def case(name):
+    if name not in _CASES:
+        _CASES[name] = Case(SMALL[name])
+    return _CASES[name]
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_population_bitexact(name):
+    c = case(name)
+    d, r = c.dev, c.ref
+    for key in ("k_codes", "v_codes", "k_scale", "k_zero", "v_scale", "v_zero"):
+        g = getattr(d, key).cpu().numpy()
+        assert np.array_equal(g.view(np.uint8), r.pool[key].view(np.uint8)), key
+    assert np.array_equal(_np16(d.k_fresh), r.k_fresh)
+    assert np.array_equal(_np16(d.v_fresh), r.v_fresh)
+    assert np.array_equal(_np16(d.q), r.q)
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_stitch_bitexact(name):
+    from paper_2608_21362_amd import kvb, pipeline
+
+    c = case(name)
+    # bf16 output, as the path runs it (rows of the stitched cache before the patch)
+    pb = pipeline.buffers(c.dev)
+    pipeline.stitch(c.dev, pb)
+    torch.cuda.synchronize()
+    assert np.array_equal(_np16(pb.k_cache), c.ref_ck)
+    assert np.array_equal(_np16(pb.v_cache), c.ref_cv)
+    # float32 output
+    w = c.w
+    shape = (len(c.layers), w.n_kv_heads, w.t_total, w.head_dim)
+    kf = torch.full(shape, float("nan"), dtype=torch.float32, device="cuda")
+    vf = torch.full_like(kf, float("nan"))
+    pipeline.stitch(c.dev, pb, out_dtype=kvb.KVB_F32, k_out=kf, v_out=vf)
+    torch.cuda.synchronize()
+    rk = np.full(shape, np.nan, np.float32)
+    rv = np.full(shape, np.nan, np.float32)
+    ostitch.stitch_into(rk, rv, c.ref.pool, c.ref.chunks, c.ref.cos, c.ref.sin, "f32")
+    gk, gv = kf.cpu().numpy(), vf.cpu().numpy()
+    assert np.array_equal(gk.view(np.uint32), rk.view(np.uint32))
+    assert np.array_equal(gv.view(np.uint32), rv.view(np.uint32))
+
+
+def _ulp32(x):
+    x = np.abs(np.asarray(x, np.float32))
+    return np.spacing(x)
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_deviation_and_selection(name):
+    c = case(name)
+    gd = c.pb.delta.cpu().numpy()
+    rd32 = c.ref_delta.astype(np.float32)
+    assert gd.shape == rd32.shape
+    assert np.all(np.abs(gd.astype(np.float64) - rd32) <= _ulp32(rd32)), "deviation beyond 1 ulp"
+    exact = float(np.mean(gd == rd32))
+    _say(f"[deviation] {name}: {exact:.6f} of rows bit-equal to the oracle")
+    rows = c.pb.rows.cpu().numpy()
+    cu = c.pb.cu_rows.cpu().numpy()
+    for si in range(gd.shape[0]):
+        r_rows, r_cu = osel.select(rd32[si], c.s.hit_row, c.forced, c.s.cu_seqlens, c.kseq)
+        g_rows = rows[si, : cu[si, -1]]
+        if np.array_equal(g_rows, r_rows) and np.array_equal(cu[si], r_cu):
+            continue
+        # only allowed where the oracle's ranking is within 1e-4 at the cut
+        margin = osel.kth_margin(rd32[si], c.s.hit_row, c.s.cu_seqlens, c.kseq)
+        assert np.any(margin <= 1e-4), f"set {si}: selection differs with margins {margin}"
+        diff = np.setxor1d(g_rows, r_rows)
+        for b in range(len(c.s.cu_seqlens) - 1):
+            lo, hi = c.s.cu_seqlens[b], c.s.cu_seqlens[b + 1]
+            cand = [r for r in range(lo, hi) if c.s.hit_row[r]]
+            order = osel.top_k(rd32[si], cand, len(cand))
+            k = int(c.kseq[b])
+            if 0 < k < len(order):
+                kth = float(rd32[si][order[k - 1]])
+                for r in diff[(diff >= lo) & (diff < hi)]:
+                    assert abs(float(rd32[si][r]) - kth) <= 1e-4
+        assert np.all(np.diff(g_rows) > 0)
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_patch_and_attention(name):
+    from paper_2608_21362_amd import kvb
+
+    c = case(name)
+    w = c.w
+    rows = c.pb.rows.cpu().numpy()
+    cu = c.pb.cu_rows.cpu().numpy()
+    gk, gv = _np16(c.pb.k_cache), _np16(c.pb.v_cache)
+    out = _np16(c.pb.out)
+    rd32 = c.ref_delta.astype(np.float32)
+    for i in range(len(c.layers)):
+        si = i if w.per_layer else 0
+        r_rows, _ = osel.select(rd32[si], c.s.hit_row, c.forced, c.s.cu_seqlens, c.kseq)
+        g_rows = rows[si, : cu[si, -1]]
+        if not np.array_equal(r_rows, g_rows):
+            pytest.skip("selection differs inside the 1e-4 margin band; attention compared elsewhere")
+        # patch
+        pk = oatt.patch(c.ref_ck[i], c.ref.k_fresh[i], r_rows)
+        pv = oatt.patch(c.ref_cv[i], c.ref.v_fresh[i], r_rows)
+        assert np.array_equal(gk[i], pk) and np.array_equal(gv[i], pv)
+        # attention on the selected rows
+        ref = oatt.attend_rows(c.ref.q[i], pk, pv, r_rows, c.s.cu_seqlens)
+        got = numerics.bf16_bits_to_f32(out[i][r_rows]).astype(np.float64)
+        err = np.abs(got - ref)
+        bad = err > ATOL + RTOL * np.abs(ref)
+        _say(f"[attention] {name} layer {i}: rows {len(r_rows)} max|err| {err.max():.3e} "
+             f"rel-fro {np.linalg.norm(got - ref) / np.linalg.norm(ref):.3e}")
+        assert not bad.any(), f"{bad.sum()} elements outside tolerance, worst {err.max()}"
+        others = np.setdiff1d(np.arange(w.t_total), r_rows)
+        assert np.all(out[i][others] == 0xFFFF)
+
+
+def test_select_stage_isolated_with_ties():
+    """Selection alone on generator-drawn deviations with exact ties, -0/+0
+    and several prompts and sets: bit-exact with the oracle."""
+    _need_gpu()
+    from paper_2608_21362_amd import kvb
+
+    rng = np.random.default_rng(21)
+    lens = [700, 1, 2048, 333, 1500]
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    T, B, n_sets = int(cu[-1]), len(lens), 3
+    flags = np.zeros(T, np.uint8)
+    cand = rng.random(T) < 0.8
+    flags[cand] |= 1
+    forced = (~cand) | (rng.random(T) < 0.05)
+    flags[forced] |= 2
+    for levels in (0, 5, 40):
+        delta = kw.deviation_draw(n_sets, T, seed=levels, n_levels=levels)
+        ks = []
+        for si in range(n_sets):
+            kk = osel.k_per_prompt(cu, cand, 15 + 10 * si, 100)
+            ks.append(kk)
+        ks = np.array(ks, np.int32)
+        ks[2, 1] = 5  # more than the prompt's candidates: takes them all
+        ws_bytes = kvb.kvb_select_workspace_bytes(n_sets, T, B)
+        d_delta = torch.from_numpy(delta).cuda()
+        d_flags = torch.from_numpy(flags).cuda()
+        d_k = torch.from_numpy(ks).cuda()
+        d_cu = torch.from_numpy(cu).cuda()
+        d_rows = torch.full((n_sets, T), -1, dtype=torch.int32, device="cuda")
+        d_cur = torch.zeros((n_sets, B + 1), dtype=torch.int32, device="cuda")
+        ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device="cuda")
+        kvb.kvb_select(n_sets, T, d_cu, B, d_delta, d_flags, d_k, d_rows, d_cur, ws, ws_bytes)
+        torch.cuda.synchronize()
+        g_rows, g_cu = d_rows.cpu().numpy(), d_cur.cpu().numpy()
+        for si in range(n_sets):
+            r_rows, r_cu = osel.select(delta[si], cand, forced, cu, np.minimum(ks[si], 10**9))
+            assert np.array_equal(g_cu[si], r_cu), (levels, si)
+            assert np.array_equal(g_rows[si, : r_cu[-1]], r_rows), (levels, si)
+
+
+def test_attention_stage_isolated_generator_rows():
+    """Attention alone on a generator-drawn row subset (both sides patch the
+    same rows): several prompts, ragged tiles, a split key range."""
+    _need_gpu()
+    from paper_2608_21362_amd import kvb, pipeline
+
+    w = kw.scaled(kw.WORKLOADS["batched_mixed"], n_prompts=2, chunks_per_prompt=24)
+    s = kw.structure(w)
+    dev = pipeline.populate(w, s)
+    ref = opop.populate(w, s)
+    rows = kw.row_subset(w, s, 900, seed=5)
+    cu_rows = np.searchsorted(rows, s.cu_seqlens).astype(np.int32)
+    T, B = w.t_total, len(s.cu_seqlens) - 1
+    d_rows = torch.from_numpy(rows).cuda()
+    d_cur = torch.from_numpy(cu_rows).cuda()
+    kc, vc = dev.cache_init_k.clone(), dev.cache_init_v.clone()
+    # stitched cache first (its parity is checked elsewhere)
+    pb = pipeline.buffers(dev)
+    pipeline.stitch(dev, pb)
+    kc.copy_(pb.k_cache)
+    vc.copy_(pb.v_cache)
+    out = torch.full((1, T, w.n_q_heads, w.head_dim), -1, dtype=torch.int16, device="cuda")
+    max_seq = int(np.max(np.diff(s.cu_seqlens)))
+    wsb = kvb.kvb_sparse_attn_workspace_bytes(1, w.n_q_heads, w.n_kv_heads, w.head_dim, T, B,
+                                              max_seq, len(rows))
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+    kvb.kvb_sparse_attn(1, w.n_q_heads, w.n_kv_heads, w.head_dim, T, dev.cu_seqlens, B, max_seq,
+                        d_rows, d_cur, 0, len(rows), dev.q, dev.k_fresh, dev.v_fresh, kc, vc,
+                        1.0 / np.sqrt(w.head_dim), kvb.KVB_BF16, out, ws, wsb)
+    torch.cuda.synchronize()
+    ck, cv = ref.cache_k.copy(), ref.cache_v.copy()
+    ostitch.stitch_into(ck, cv, ref.pool, ref.chunks, ref.cos, ref.sin, "bf16")
+    pk = oatt.patch(ck[0], ref.k_fresh[0], rows)
+    pv = oatt.patch(cv[0], ref.v_fresh[0], rows)
+    assert np.array_equal(_np16(kc)[0], pk) and np.array_equal(_np16(vc)[0], pv)
+    refo = oatt.attend_rows(ref.q[0], pk, pv, rows, s.cu_seqlens)
+    got = numerics.bf16_bits_to_f32(_np16(out)[0][rows]).astype(np.float64)
+    err = np.abs(got - refo)
+    _say(f"[attention-isolated] rows {len(rows)} max|err| {err.max():.3e} ws {wsb}")
+    assert np.all(err <= ATOL + RTOL * np.abs(refo))
