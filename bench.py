@@ -1,0 +1,232 @@
+"""Benchmark of the stitched-prefill path on one MI355X.
+
+One step = one pass of the whole path over one 8K-token prompt of the
+36-layer Qwen2.5-3B-shaped workload (16 query / 2 KV heads, d = 128, int4
+KIVI pool with 64 cached chunks at random original offsets, 15 % per-layer
+recompute):
+
+    kvb_stitch (all layers, one launch)
+    kvb_deviation_topk (all layers, one call: deviation + selection)
+    kvb_sparse_attn x 36 (one launch per layer, as a model runs its layers)
+
+Inputs are resident in HBM before the timed region.  Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                    [--attn-all-layers] [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 / fp16 MFMA
+METRIC = "stitched-prefill tokens/s + HBM GB/s / MFMA util, Qwen2.5-3B shape 8K ctx"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic(w, s, rows_per_set, cu_rows_per_set):
+    """Algorithmic work of one step (bytes a kernel must move, flops it must do)."""
+    L, H, d, C, T, Hq = w.n_layers, w.n_kv_heads, w.head_dim, w.chunk_len, w.t_total, w.n_q_heads
+    P = s.n_pool
+    cb = d * w.bits // 8
+    codes = 2 * P * L * H * C * cb
+    stats = P * L * H * (C // w.k_group) * d * 8 + P * L * H * C * (d // w.v_group) * 8
+    stitch_out = 2 * P * L * H * C * d * 2
+    stitch_bytes = codes + stats + stitch_out
+    n_sets = rows_per_set.shape[0]
+    dev_bytes = 2 * L * H * T * d * 2 + n_sets * T * 4
+    pos = s.positions().astype(np.int64)
+    flops_per_layer = []
+    for l in range(L):
+        si = l if w.per_layer else 0
+        r = rows_per_set[si, : cu_rows_per_set[si, -1]]
+        flops_per_layer.append(4.0 * d * Hq * float(np.sum(pos[r] + 1)))
+    return stitch_bytes, dev_bytes, np.array(flops_per_layer)
+
+
+def cpu_baseline(w, s, n_layers_sample):
+    """The oracle as it stands, on the first ``n_layers_sample`` layers of the
+    same workload; scaled to the whole step linearly in layers."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import path as opath
+    from oracle import populate as opop
+
+    layers = list(range(n_layers_sample))
+    pop = opop.populate(w, s, layers=layers)
+    t0 = time.perf_counter()
+    opath.run(w, s, pop)
+    dt = time.perf_counter() - t0
+    per_step = dt / n_layers_sample * w.n_layers
+    blas = [i.get("num_threads", 1) for i in threadpool_info()]
+    return {
+        "value": w.t_total / per_step, "unit": "tokens/s",
+        "cores": int(max(blas) if blas else 1), "kind": "oracle",
+        "sample": f"{n_layers_sample} of {w.n_layers} layers, every selected row "
+                  f"(stitch, deviation, selection, patch, attention), {dt:.1f} s of CPU time; "
+                  f"scaled to {w.n_layers} layers",
+        "seconds": dt,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="qwen_36l_8k")
+    ap.add_argument("--attn-all-layers", action="store_true",
+                    help="one attention launch for all layers (ceiling variant)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-layers", type=int, default=20)
+    ap.add_argument("--flush-mb", type=int, default=512)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the path runs on a single MI355X and no "
+              "multi-GPU variant is built (use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import kvb_workload as kw
+    from paper_2608_21362_amd import pipeline
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w = kw.WORKLOADS[args.workload]
+    s = kw.structure(w)
+    log(f"[bench] workload {w.name}: L={w.n_layers} T={w.t_total} chunks={s.n_pool} "
+        f"bits={w.bits}; populating on the GPU")
+    t0 = time.time()
+    di = pipeline.populate(w, s)
+    pb = pipeline.buffers(di, attn_all_layers=args.attn_all_layers)
+    torch.cuda.synchronize()
+    log(f"[bench] inputs resident ({time.time() - t0:.1f} s)")
+
+    stream = torch.cuda.current_stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    L = di.n_layers
+
+    def step(rec=None):
+        if rec is not None:
+            rec[0].record(stream)
+        pipeline.stitch(di, pb)
+        if rec is not None:
+            rec[1].record(stream)
+        pipeline.deviation_topk(di, pb)
+        if rec is not None:
+            rec[2].record(stream)
+        if args.attn_all_layers:
+            pipeline.sparse_attn_all(di, pb)
+            if rec is not None:
+                rec[3].record(stream)
+        else:
+            for i in range(L):
+                pipeline.sparse_attn_layer(di, pb, i)
+                if rec is not None:
+                    rec[3 + i].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    n_ev = 3 + (1 if args.attn_all_layers else L)
+    recs = [[ev() for _ in range(n_ev)] for _ in range(args.steps)]
+    start, stop = ev(), ev()
+    torch.cuda.synchronize()
+    start.record(stream)
+    for k in range(args.steps):
+        step(recs[k])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    ms_step = total_ms / args.steps
+    st_ms = np.mean([r[0].elapsed_time(r[1]) for r in recs])
+    dv_ms = np.mean([r[1].elapsed_time(r[2]) for r in recs])
+    at_ms = np.array([[r[2 + j].elapsed_time(r[3 + j]) for j in range(n_ev - 3)] for r in recs])
+    attn_ms_launch = float(at_ms.mean())
+
+    rows = pb.rows.cpu().numpy()
+    cu = pb.cu_rows.cpu().numpy()
+    st_bytes, dev_bytes, flops = algorithmic(w, s, rows, cu)
+    attn_flops_launch = float(flops.mean()) if not args.attn_all_layers else float(flops.sum())
+    attn_tflops = attn_flops_launch / (attn_ms_launch * 1e-3) / 1e12
+
+    # stitch and deviation bandwidth with the 256 MiB Infinity Cache flushed between reps
+    flush = torch.empty(args.flush_mb << 20, dtype=torch.uint8, device="cuda")
+    st_f, dv_f = [], []
+    for _ in range(5):
+        flush.fill_(1)
+        a, b, c = ev(), ev(), ev()
+        a.record(stream)
+        pipeline.stitch(di, pb)
+        b.record(stream)
+        torch.cuda.synchronize()
+        flush.fill_(2)
+        b2 = ev()
+        b2.record(stream)
+        pipeline.deviation_topk(di, pb)
+        c.record(stream)
+        torch.cuda.synchronize()
+        st_f.append(a.elapsed_time(b))
+        dv_f.append(b2.elapsed_time(c))
+    del flush
+    st_gbs = st_bytes / (np.median(st_f) * 1e-3) / 1e9
+    dv_gbs = dev_bytes / (np.median(dv_f) * 1e-3) / 1e9
+
+    tokens_per_step = w.t_total
+    result = {
+        "metric": METRIC,
+        "value": tokens_per_step / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded draws with the workload's shapes and distributions)",
+        "config": {
+            "workload": w.name, "layers": w.n_layers, "prompt_tokens": w.t_total,
+            "q_heads": w.n_q_heads, "kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
+            "kivi_bits": w.bits, "k_group": w.k_group, "v_group": w.v_group,
+            "cached_chunks": s.n_pool, "recompute": f"{w.rho_num}/{w.rho_den} per layer",
+            "attention_launches": "one per layer" if not args.attn_all_layers else "one for all layers",
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "kernel": "kvb_sparse_attn (patch + attention + split combine) per launch",
+            "bound": "mfma", "achieved": attn_tflops, "peak": MFMA_BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": attn_tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": None,
+            "flops_per_launch": attn_flops_launch, "ms_per_launch": attn_ms_launch,
+        },
+        "kernels": {
+            "stitch_ms": float(st_ms), "deviation_topk_ms": float(dv_ms),
+            "sparse_attn_ms_per_step": float(at_ms.sum(axis=1).mean()),
+            "stitch_GBps_flushed": st_gbs, "stitch_hbm_frac": st_gbs / HBM_PEAK_GBS,
+            "stitch_bytes": st_bytes,
+            "deviation_topk_GBps_flushed": dv_gbs, "deviation_hbm_frac": dv_gbs / HBM_PEAK_GBS,
+            "deviation_bytes": dev_bytes,
+            "selected_rows_per_layer": float(np.mean(cu[:, -1])),
+        },
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] cpu baseline: oracle on {args.cpu_layers} layers")
+        result["cpu_baseline"] = cpu_baseline(w, s, args.cpu_layers)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
