@@ -91,6 +91,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=20)
     ap.add_argument("--flush-mb", type=int, default=512)
+    ap.add_argument("--calibrate-copy-mb", type=int, default=0,
+                    help="also run one plain device copy of this size (counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -183,6 +185,14 @@ def main():
     del flush
     st_gbs = st_bytes / (np.median(st_f) * 1e-3) / 1e9
     dv_gbs = dev_bytes / (np.median(dv_f) * 1e-3) / 1e9
+
+    if args.calibrate_copy_mb:
+        src = torch.ones(args.calibrate_copy_mb << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     tokens_per_step = w.t_total
     result = {

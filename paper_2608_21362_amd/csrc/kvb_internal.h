@@ -44,7 +44,9 @@ struct AttnPlan {
   int tile_slots;      // tile slots per (layer, kv head)
   int split_len;       // keys per split (multiple of the key block)
   int n_split_max;     // splits per tile slot
-  size_t workspace;    // bytes of split partials
+  size_t v16_offset;   // workspace offset of the fp16 copy of V
+  size_t parts_offset; // workspace offset of the split partials
+  size_t workspace;    // total workspace bytes
 };
 bool attn_plan(int n_layers, int n_q_heads, int n_kv_heads, int head_dim, int64_t t_total,
                int n_seqs, int max_seq_len, int max_rows, AttnPlan* plan);

@@ -1,33 +1,43 @@
 // Patch and sparse-query causal GQA attention (Alg. 2 step 4; Eq. 2).
 //
-// patch_kernel: cache[l][h][t] <- fresh[l][h][t] for every selected row t,
-// both tensors, every kv head (one wave per row).
+// Per layer the call runs four kernels on one stream:
+//
+//   patch_kernel     cache[l][h][t] <- fresh[l][h][t] for every selected row t
+//                    (both tensors, every kv head; one wave per row)
+//   v16_kernel       the patched V of the layer converted to fp16 in the
+//                    workspace (exact for |v| <= 65504: a bf16 significand fits
+//                    an fp16 one), so the P.V product can take fp16 operands
+//                    straight from LDS
+//   attn_kernel      the attention itself (below)
+//   combine_kernel   merges KV-split partials in split order (only when a
+//                    tile's key range was split)
 //
 // attn_kernel: one workgroup = one (layer, kv head g, tile of selected rows,
 // KV split).  The tile packs rows x the G = Hq/Hkv query heads that share kv
 // head g into the MFMA N dimension: each of the 4 waves owns 32 query vectors
-// (32/G rows x G heads).  Keys stream through LDS in blocks of 64:
+// (32/G rows x G heads).  Keys stream in blocks of 64 through a two-stage LDS
+// ring filled by asynchronous global->LDS loads (no VGPR staging), XOR-swizzled
+// on 16-byte chunks so the operand reads below are free of bank conflicts:
 //
-//   S^T (64 keys x 32 queries) = K Q^T      bf16 MFMA 32x32x16 (K from LDS as
-//                                            the A operand, Q^T held in VGPRs)
-//   online softmax over keys                fp32, base-2 exponent; each lane
-//                                            holds 32 scores of one query, the
-//                                            other 32 sit in lane ^ 32
-//   O^T (d x 32 queries) += V^T P^T         fp16 MFMA 32x32x16 (V^T from LDS,
-//                                            P^T straight from the S^T
-//                                            accumulators)
+//   S^T (64 keys x 32 queries) = K Q^T     bf16 MFMA 32x32x16: K rows from LDS
+//                                           (A operand), Q^T kept in VGPRs
+//   online softmax over keys               fp32, base-2 exponent.  Each lane
+//                                           holds 32 scores of one query, the
+//                                           other 32 sit in lane ^ 32.  The
+//                                           running maximum is refreshed only
+//                                           when a block raises it by more
+//                                           than 8 (log2 units), so partial
+//                                           probabilities stay below 2^8
+//   O^T (d x 32 queries) += V^T P^T        fp16 MFMA 32x32x16: V^T read from
+//                                           the row-major fp16 V block with the
+//                                           LDS transpose read, P^T converted
+//                                           from the S^T accumulators
 //
-// V is stored in LDS transposed ([d][key], fp16) with the keys of every
-// 16-key group permuted so that the 8 keys a lane contributes to one P^T
-// operand (the accumulator layout gives lane half h the keys
-// {4h..4h+3, 8+4h..8+4h+3}) are 16 contiguous bytes.  The contraction
-// dimension of both products is only ever indexed consistently on the two
-// operands, so its lane order inside the MFMA does not matter.
-//
-// The next key block is loaded from HBM into registers while the current one
-// is consumed from LDS.  A tile whose key range is longer than the split
-// length is cut into splits whose (max, sum, O) partials go to the workspace
-// and are merged in split order by combine_kernel (deterministic).
+// The accumulator layout of a 32x32 MFMA gives lane half h the keys
+// {4h..4h+3, 8+4h..8+4h+3} of every 16-key step; the transpose reads fetch V
+// for exactly those keys, so no permutation is needed anywhere.  The
+// contraction index of each product is laid out identically on its two
+// operands, so its order inside the MFMA does not matter.
 #include <math.h>
 
 #include "kvb_device.h"
@@ -38,6 +48,9 @@ namespace {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
+typedef __attribute__((ext_vector_type(4))) short s16x4;
+typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
+typedef __attribute__((ext_vector_type(4))) unsigned u32x4;
 typedef __attribute__((ext_vector_type(2))) _Float16 f16x2;
 typedef __attribute__((ext_vector_type(2))) float f32x2;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
@@ -47,7 +60,21 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kQW = 32;                 // query vectors per wave
 constexpr int kQT = kQW * kWaves;       // query vectors per workgroup
 constexpr int kKB = 64;                 // keys per block
-constexpr int kVtStride = kKB + 8;      // fp16 elements per transposed-V row
+constexpr float kLazy = 8.0f;           // max growth (log2 units) tolerated before a rescale
+
+#define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
+
+// wait until at most n vector-memory operations of this wave are outstanding
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// wait until this wave's LDS operations have completed
+__device__ __forceinline__ void wait_lgkmcnt0() {
+  __builtin_amdgcn_s_waitcnt((0xF) | (0x3 << 14) | (0x7 << 4) | (0x0 << 8));
+}
 
 // ---------------------------------------------------------------- patch ----
 __global__ void __launch_bounds__(256)
@@ -79,6 +106,24 @@ patch_kernel(int32_t L, int32_t Hkv, int32_t D, int64_t t_total, int32_t n_seqs,
   }
 }
 
+// ------------------------------------------------------------ V to fp16 ----
+__device__ __forceinline__ uint32_t bf16pair_to_f16pair(uint32_t w) {
+  f32x2 f = {bf16_lo(w), bf16_hi(w)};
+  f16x2 h = __builtin_convertvector(f, f16x2);
+  return __builtin_bit_cast(uint32_t, h);
+}
+
+__global__ void __launch_bounds__(256)
+v16_kernel(int64_t n8, const uint16_t* __restrict__ v, uint16_t* __restrict__ v16) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n8;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const uint4 a = reinterpret_cast<const uint4*>(v)[i];
+    reinterpret_cast<uint4*>(v16)[i] =
+        make_uint4(bf16pair_to_f16pair(a.x), bf16pair_to_f16pair(a.y),
+                   bf16pair_to_f16pair(a.z), bf16pair_to_f16pair(a.w));
+  }
+}
+
 // ------------------------------------------------------------ tile lookup --
 struct Tile {
   int b;          // prompt
@@ -103,13 +148,199 @@ __device__ __forceinline__ bool find_tile(const int32_t* cur, int n_seqs, int ro
   return false;
 }
 
-__device__ __forceinline__ uint32_t bf16pair_to_f16pair(uint32_t w) {
-  f32x2 f = {bf16_lo(w), bf16_hi(w)};
-  f16x2 h = __builtin_convertvector(f, f16x2);
-  return __builtin_bit_cast(uint32_t, h);
+// ---------------------------------------------------------------- attention
+template <int D>
+struct AttnCfg {
+  static constexpr int ROWB = D * 2;                 // bytes per K / V16 row
+  static constexpr int CPR = ROWB / 16;              // 16-byte chunks per row
+  static constexpr int BLK = kKB * ROWB;             // bytes of one K (or V) block
+  static constexpr int RPI = 1024 / ROWB;            // rows per wave-wide 1 KiB load
+  static constexpr int LOADS = BLK / (kThreads * 16);  // per-thread loads per tensor per block
+  static constexpr int NS = D / 16;                  // 16-deep MFMA steps over d
+  static constexpr int ND = D / 32;                  // 32-row d tiles of O^T
+  // 16-byte-chunk swizzles (slot = chunk ^ f(row))
+  static __device__ __forceinline__ int swz_k(int r) { return r % CPR; }
+  static __device__ __forceinline__ int swz_v(int r) { return (CPR / 4) * (r & 3); }
+};
+
+// Per-lane byte offsets (inside a block) of this thread's asynchronous loads:
+// piece i of the block is the 1 KiB a wave writes with one instruction; lane L
+// writes LDS bytes 16 L of it, i.e. row piece*RPI + L/CPR, slot L % CPR, and
+// fetches the global chunk that the swizzle maps to that slot.
+template <int D>
+struct LoadOffsets {
+  int k[AttnCfg<D>::LOADS];
+  int v[AttnCfg<D>::LOADS];
+};
+
+template <int D>
+__device__ __forceinline__ LoadOffsets<D> load_offsets(int wave, int lane) {
+  using C = AttnCfg<D>;
+  LoadOffsets<D> o;
+#pragma unroll
+  for (int i = 0; i < C::LOADS; ++i) {
+    const int r = (wave * C::LOADS + i) * C::RPI + lane / C::CPR;
+    const int slot = lane % C::CPR;
+    o.k[i] = r * C::ROWB + 16 * (slot ^ C::swz_k(r));
+    o.v[i] = r * C::ROWB + 16 * (slot ^ C::swz_v(r));
+  }
+  return o;
 }
 
-// ---------------------------------------------------------------- attention
+// Raw buffer resource (128-bit, stride 0) over `bytes` bytes at `base`; loads
+// at offsets >= bytes return zero.
+typedef __attribute__((ext_vector_type(4))) int i32x4;
+__device__ __forceinline__ i32x4 buffer_rsrc(const void* base, int bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xFFFFu));
+  r[2] = __builtin_amdgcn_readfirstlane(bytes);
+  r[3] = 0x00020000;
+  return r;
+}
+
+// One asynchronous 16-byte-per-lane load from a buffer straight into LDS: lane
+// L's data lands at lds_addr + 16 L.  Issued as inline assembly so the compiler
+// does not order LDS reads of the *other* ring stage behind it; completion is
+// awaited explicitly with wait_vmcnt before the stage is read.
+__device__ __forceinline__ void lds_dma16(i32x4 rsrc, uint32_t lds_addr, int voff, int soff) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %1, %2, %3 offen lds"
+      :
+      : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
+      : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)LDS_PTR(const char, p);
+}
+
+// Issue the asynchronous loads of one 64-key block of K (bf16) and V (fp16)
+// into one LDS stage.  The buffer resources cover exactly the cache rows of
+// this (layer, kv head); rows past the end read as zero (their scores are
+// masked).
+template <int D>
+__device__ __forceinline__ void issue_block(i32x4 krs, i32x4 vrs, int kb, const LoadOffsets<D>& lo,
+                                            char* k_st, char* v_st, int wave) {
+  using C = AttnCfg<D>;
+  // the block offset goes into the lane offset: the buffer range check covers
+  // the lane offset, not the scalar one
+  const int boff = kb * C::ROWB;
+  const uint32_t kbase = __builtin_amdgcn_readfirstlane(lds_addr(k_st) + wave * C::LOADS * 1024);
+  const uint32_t vbase = __builtin_amdgcn_readfirstlane(lds_addr(v_st) + wave * C::LOADS * 1024);
+#pragma unroll
+  for (int i = 0; i < C::LOADS; ++i) {
+    lds_dma16(krs, kbase + i * 1024, boff + lo.k[i], 0);
+    lds_dma16(vrs, vbase + i * 1024, boff + lo.v[i], 0);
+  }
+}
+
+template <int D>
+struct AttnState {
+  f32x16 o[AttnCfg<D>::ND];
+  float m_raw;   // running maximum of raw scores (stale by at most kLazy / scale)
+  float l_part;  // this lane's share of the running sum
+};
+
+template <int D>
+__device__ __forceinline__ void attend_block(const char* k_st, const char* v_st,
+                                             const bf16x8 (&qop)[AttnCfg<D>::NS],
+                                             AttnState<D>& st, float c_log2, bool full,
+                                             int kb, int t_q, int k_hi, int lane) {
+  using C = AttnCfg<D>;
+  const int half = lane >> 5, n = lane & 31;
+  // S^T = K Q^T
+  f32x16 sacc[2];
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt) {
+    sacc[kt] = f32x16{};
+    const int r = kt * 32 + n;
+    const char* krow = k_st + r * C::ROWB;
+#pragma unroll
+    for (int s = 0; s < C::NS; ++s) {
+      const int chunk = (D / 16) * half + s;
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + 16 * (chunk ^ C::swz_k(r)));
+      sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qop[s], sacc[kt], 0, 0, 0);
+    }
+  }
+  if (!full) {
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kb + kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        if (key > t_q || key >= k_hi) sacc[kt][r] = -INFINITY;
+      }
+  }
+  float bmax = sacc[0][0];
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) bmax = fmaxf(bmax, sacc[kt][r]);
+  bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
+  const float m_new = fmaxf(st.m_raw, bmax);
+  // refresh the reference maximum only when some lane's scores grew by > kLazy
+  const bool grow = (m_new - st.m_raw) * c_log2 > kLazy || st.m_raw == -INFINITY;
+  if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+    const float alpha = (st.m_raw == -INFINITY || m_new == -INFINITY)
+                            ? (m_new == -INFINITY ? 1.0f : 0.0f)
+                            : __builtin_amdgcn_exp2f((st.m_raw - m_new) * c_log2);
+    st.l_part *= alpha;
+#pragma unroll
+    for (int dt = 0; dt < C::ND; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) st.o[dt][r] *= alpha;
+    st.m_raw = m_new;
+  }
+  const float mc = st.m_raw == -INFINITY ? 0.0f : st.m_raw * c_log2;
+  float psum = 0.0f;
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][r], c_log2, -mc));
+      sacc[kt][r] = p;
+      psum += p;
+    }
+  st.l_part += psum;
+  // O^T += V^T P^T over four 16-key steps
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const int kt = ks >> 1, r0 = 8 * (ks & 1);
+    f16x8 pb;
+#pragma unroll
+    for (int v = 0; v < 8; v += 2) {
+      const f32x2 f = {sacc[kt][r0 + v], sacc[kt][r0 + v + 1]};
+      const f16x2 h = __builtin_convertvector(f, f16x2);
+      pb[v] = h[0];
+      pb[v + 1] = h[1];
+    }
+    // transpose-read lane address: row kbase + j/4, d = dbase + 4 (j % 4)
+    const int j = lane & 15, grp = (lane >> 4) & 1;
+#pragma unroll
+    for (int dt = 0; dt < C::ND; ++dt) {
+      const int dbase = dt * 32 + 16 * grp;
+      u32x2 part[2];
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int row = ks * 16 + 8 * hh + 4 * half + (j >> 2);
+        const int elem = dbase + 4 * (j & 3);
+        const int chunk = elem >> 3;
+        const char* addr = v_st + row * C::ROWB + 16 * (chunk ^ C::swz_v(row)) + 2 * (elem & 7);
+        part[hh] = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, addr)));
+      }
+      // whole-register concatenation (keys 4h..4h+3, then 8+4h..8+4h+3); element-wise
+      // 16-bit extraction here has been miscompiled into a broadcast of element 0
+      const u32x4 w = {part[0][0], part[0][1], part[1][0], part[1][1]};
+      const f16x8 a = __builtin_bit_cast(f16x8, w);
+      st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, pb, st.o[dt], 0, 0, 0);
+    }
+  }
+}
+
 template <int D>
 __global__ void __launch_bounds__(kThreads, 2)
 attn_kernel(int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total,
@@ -117,15 +348,13 @@ attn_kernel(int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total,
             const int32_t* __restrict__ rows, const int32_t* __restrict__ cu_rows,
             int32_t rows_per_layer, int32_t rows_per_tile, int32_t tile_slots, int32_t split_len,
             int32_t n_split_max, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
-            const uint16_t* __restrict__ vc, float scale_log2, int32_t out_f32,
+            const uint16_t* __restrict__ v16, float c_log2, int32_t out_f32,
             void* __restrict__ out, float* __restrict__ ws) {
-  constexpr int NS = D / 16;        // bf16 MFMA steps over d
-  constexpr int ND = D / 32;        // 32-row tiles of d in O^T
-  constexpr int KS = D + 8;         // bf16 elements per K row in LDS
-  constexpr int KCH = D / 8;        // 16-byte chunks per K row
-  constexpr int KLD = kKB * KCH / kThreads;  // K chunks per thread per block
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kKB * KS];
-  __shared__ __attribute__((aligned(16))) uint16_t vt_lds[D * kVtStride];
+  using C = AttnCfg<D>;
+  __shared__ __attribute__((aligned(1024))) char k_st0[C::BLK];
+  __shared__ __attribute__((aligned(1024))) char k_st1[C::BLK];
+  __shared__ __attribute__((aligned(1024))) char v_st0[C::BLK];
+  __shared__ __attribute__((aligned(1024))) char v_st1[C::BLK];
 
   const int G = 1 << log2g;
   const int lg = blockIdx.z;
@@ -136,183 +365,101 @@ attn_kernel(int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total,
   const int32_t* rws = rows + set * t_total;
   Tile tile;
   if (!find_tile(cur, n_seqs, rows_per_tile, slot, &tile)) return;
-  const int64_t kstart = cu_seqlens[tile.b];
-  const int64_t kend = min((int64_t)rws[tile.r_end - 1] + 1, t_total);
+  const int T = (int)t_total;
+  const int kstart = cu_seqlens[tile.b];
+  const int kend = min(rws[tile.r_end - 1] + 1, T);
   if (kend <= kstart) return;
-  const int n_split = (int)((kend - kstart + split_len - 1) / split_len);
+  const int n_split = (kend - kstart + split_len - 1) / split_len;
   if (split >= n_split || n_split > n_split_max) return;
-  const int64_t k_lo = kstart + (int64_t)split * split_len;
-  const int64_t k_hi = min(k_lo + (int64_t)split_len, kend);
-  const int64_t t_min = rws[tile.r_begin];
+  const int k_lo = kstart + split * split_len;
+  const int k_hi = min(k_lo + split_len, kend);
+  const int t_min = rws[tile.r_begin];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5, n = lane & 31;
   const int rows_per_wave = kQW >> log2g;
   const int row_idx = tile.r_begin + wave * rows_per_wave + (n >> log2g);
   const int head = g * G + (n & (G - 1));
-  int64_t t_q = row_idx < tile.r_end ? (int64_t)rws[row_idx] : -1;
+  int t_q = row_idx < tile.r_end ? rws[row_idx] : -1;
   const bool qvalid = t_q >= kstart && t_q < kend;  // rows outside the prompt are skipped
   if (!qvalid) t_q = -1;
 
-  // Q^T operand: query n, d = (D/2)*half + 8s + v
-  bf16x8 qop[NS];
+  const int64_t kv_base = ((int64_t)l * Hkv + g) * t_total * D;
+  const i32x4 krs = buffer_rsrc(kc + kv_base, T * C::ROWB);
+  const i32x4 vrs = buffer_rsrc(v16 + kv_base, T * C::ROWB);
+  const LoadOffsets<D> lo = load_offsets<D>(wave, lane);
+  const int nblk = (k_hi - k_lo + kKB - 1) / kKB;
+
+  issue_block<D>(krs, vrs, k_lo, lo, k_st0, v_st0, wave);
+
+  // Q^T operand: query n, d = (D/2) h + 8 s + v
+  bf16x8 qop[C::NS];
   {
-    const uint16_t* qp = q + (((int64_t)l * t_total + (qvalid ? t_q : 0)) * Hq + head) * D +
-                         (D / 2) * half;
+    const uint16_t* qrow = q + (((int64_t)l * t_total + (qvalid ? t_q : 0)) * Hq + head) * D +
+                           (D / 2) * half;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      uint4 w = qvalid ? *reinterpret_cast<const uint4*>(qp + 8 * s) : make_uint4(0, 0, 0, 0);
+    for (int s = 0; s < C::NS; ++s) {
+      const uint4 w = qvalid ? *reinterpret_cast<const uint4*>(qrow + 8 * s) : make_uint4(0, 0, 0, 0);
       qop[s] = __builtin_bit_cast(bf16x8, w);
     }
   }
+  // Q (and the first block) must have landed before the loop: this keeps the
+  // compiler from waiting on the queries -- and so on the in-flight prefetch --
+  // inside the loop.
+  wait_vmcnt<0>();
 
-  const int64_t kv_base = ((int64_t)l * Hkv + g) * t_total;
-  const uint16_t* kb_ptr = kc + kv_base * D;
-  const uint16_t* vb_ptr = vc + kv_base * D;
-
-  // register stage of one key block
-  uint4 kreg[KLD];
-  uint4 vreg[4];
-  const bool v_job = tid < 16 * KCH;  // (key quad, 8-channel group) jobs
-  const int kq = tid & 15, dg = tid >> 4;
-  auto load_block = [&](int64_t kb) {
+  AttnState<D> st;
 #pragma unroll
-    for (int i = 0; i < KLD; ++i) {
-      const int ci = tid + kThreads * i;
-      int64_t key = kb + ci / KCH;
-      key = key < t_total ? key : t_total - 1;
-      kreg[i] = *reinterpret_cast<const uint4*>(kb_ptr + key * D + (ci % KCH) * 8);
+  for (int dt = 0; dt < C::ND; ++dt) st.o[dt] = f32x16{};
+  st.m_raw = -INFINITY;
+  st.l_part = 0.0f;
+
+  for (int jb = 0; jb < nblk; jb += 2) {
+    // even block: stage 0 (next block goes to stage 1)
+    {
+      const int kb = k_lo + jb * kKB;
+      if (jb + 1 < nblk) {
+        issue_block<D>(krs, vrs, kb + kKB, lo, k_st1, v_st1, wave);
+        wait_vmcnt<2 * C::LOADS>();
+      } else {
+        wait_vmcnt<0>();
+      }
+      __builtin_amdgcn_s_barrier();
+      const bool full = (kb + kKB - 1 <= t_min) && (kb + kKB <= k_hi);
+      attend_block<D>(k_st0, v_st0, qop, st, c_log2, full, kb, t_q, k_hi, lane);
+      wait_lgkmcnt0();
+      __builtin_amdgcn_s_barrier();
     }
-    if (v_job) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        int64_t key = kb + 4 * kq + r;
-        key = key < t_total ? key : t_total - 1;
-        vreg[r] = *reinterpret_cast<const uint4*>(vb_ptr + key * D + dg * 8);
+    if (jb + 1 < nblk) {
+      // odd block: stage 1 (next block goes to stage 0)
+      const int kb = k_lo + (jb + 1) * kKB;
+      if (jb + 2 < nblk) {
+        issue_block<D>(krs, vrs, kb + kKB, lo, k_st0, v_st0, wave);
+        wait_vmcnt<2 * C::LOADS>();
+      } else {
+        wait_vmcnt<0>();
       }
-    }
-  };
-  auto store_block = [&]() {
-#pragma unroll
-    for (int i = 0; i < KLD; ++i) {
-      const int ci = tid + kThreads * i;
-      *reinterpret_cast<uint4*>(&k_lds[(ci / KCH) * KS + (ci % KCH) * 8]) = kreg[i];
-    }
-    if (v_job) {
-      // key quad kq -> position base inside its 16-key group
-      const int run = kq & 3;
-      const int pos = (kq >> 2) * 16 + ((run == 1) ? 8 : (run == 2) ? 4 : (run == 3) ? 12 : 0);
-      const uint32_t w[4][4] = {{vreg[0].x, vreg[0].y, vreg[0].z, vreg[0].w},
-                                {vreg[1].x, vreg[1].y, vreg[1].z, vreg[1].w},
-                                {vreg[2].x, vreg[2].y, vreg[2].z, vreg[2].w},
-                                {vreg[3].x, vreg[3].y, vreg[3].z, vreg[3].w}};
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        // channel dg*8 + j of keys 4kq .. 4kq+3
-        uint32_t e[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) e[r] = (j & 1) ? (w[r][j >> 1] >> 16) : (w[r][j >> 1] & 0xFFFFu);
-        const uint32_t p01 = bf16pair_to_f16pair(e[0] | (e[1] << 16));
-        const uint32_t p23 = bf16pair_to_f16pair(e[2] | (e[3] << 16));
-        *reinterpret_cast<uint2*>(&vt_lds[(dg * 8 + j) * kVtStride + pos]) = make_uint2(p01, p23);
-      }
-    }
-  };
-
-  f32x16 o[ND];
-#pragma unroll
-  for (int dt = 0; dt < ND; ++dt) o[dt] = f32x16{};
-  float m_run = -INFINITY, l_run = 0.0f;
-
-  int64_t kb = k_lo;
-  load_block(kb);
-  for (; kb < k_hi; kb += kKB) {
-    __syncthreads();
-    store_block();
-    __syncthreads();
-    if (kb + kKB < k_hi) load_block(kb + kKB);
-
-    // S^T = K Q^T for keys kb .. kb+63
-    f32x16 sacc[2];
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      sacc[kt] = f32x16{};
-      const uint16_t* krow = &k_lds[(kt * 32 + n) * KS + (D / 2) * half];
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + 8 * s);
-        sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qop[s], sacc[kt], 0, 0, 0);
-      }
-    }
-
-    // mask, scale to log2 units, block max
-    const bool full = (kb + kKB - 1 <= t_min) && (kb + kKB <= k_hi);
-    float bmax = -INFINITY;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float v = sacc[kt][r] * scale_log2;
-        if (!full) {
-          const int64_t key = kb + kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          if (key > t_q || key >= k_hi) v = -INFINITY;
-        }
-        sacc[kt][r] = v;
-        bmax = fmaxf(bmax, v);
-      }
-    bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
-    const float m_new = fmaxf(m_run, bmax);
-    const float m_use = (m_new == -INFINITY) ? 0.0f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    float bsum = 0.0f;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = __builtin_amdgcn_exp2f(sacc[kt][r] - m_use);
-        sacc[kt][r] = p;
-        bsum += p;
-      }
-    bsum += __shfl_xor(bsum, 32, 64);
-    l_run = l_run * alpha + bsum;
-    m_run = m_new;
-#pragma unroll
-    for (int dt = 0; dt < ND; ++dt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
-
-    // O^T += V^T P^T, four 16-key steps
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int kt = ks >> 1, r0 = 8 * (ks & 1);
-      f16x8 pb;
-#pragma unroll
-      for (int v = 0; v < 8; v += 2) {
-        f32x2 f = {sacc[kt][r0 + v], sacc[kt][r0 + v + 1]};
-        f16x2 h = __builtin_convertvector(f, f16x2);
-        pb[v] = h[0];
-        pb[v + 1] = h[1];
-      }
-#pragma unroll
-      for (int dt = 0; dt < ND; ++dt) {
-        const f16x8 a = *reinterpret_cast<const f16x8*>(
-            &vt_lds[(dt * 32 + n) * kVtStride + ks * 16 + 8 * half]);
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, pb, o[dt], 0, 0, 0);
-      }
+      __builtin_amdgcn_s_barrier();
+      const bool full = (kb + kKB - 1 <= t_min) && (kb + kKB <= k_hi);
+      attend_block<D>(k_st1, v_st1, qop, st, c_log2, full, kb, t_q, k_hi, lane);
+      wait_lgkmcnt0();
+      __builtin_amdgcn_s_barrier();
     }
   }
 
   if (!qvalid) return;
+  const float l_run = st.l_part + __shfl_xor(st.l_part, 32, 64);
   if (n_split == 1) {
     const float inv = (l_run > 0.0f) ? 1.0f / l_run : 0.0f;
     const int64_t ob = (((int64_t)l * t_total + t_q) * Hq + head) * D;
 #pragma unroll
-    for (int dt = 0; dt < ND; ++dt)
+    for (int dt = 0; dt < C::ND; ++dt)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int d0 = dt * 32 + 8 * j + 4 * half;
-        const float a0 = o[dt][4 * j] * inv, a1 = o[dt][4 * j + 1] * inv;
-        const float a2 = o[dt][4 * j + 2] * inv, a3 = o[dt][4 * j + 3] * inv;
+        const float a0 = st.o[dt][4 * j] * inv, a1 = st.o[dt][4 * j + 1] * inv;
+        const float a2 = st.o[dt][4 * j + 2] * inv, a3 = st.o[dt][4 * j + 3] * inv;
         if (out_f32) {
           *reinterpret_cast<float4*>(reinterpret_cast<float*>(out) + ob + d0) =
               make_float4(a0, a1, a2, a3);
@@ -322,25 +469,29 @@ attn_kernel(int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total,
         }
       }
   } else {
+    // partial (unnormalised O, running max in log2 units, sum) of this split
     const int64_t item = ((int64_t)lg * tile_slots + slot) * n_split_max + split;
-    float* wp = ws + (item * kQT + wave * kQW + n) * (D + 2);
+    const int qi = wave * kQW + n;
+    float* wo = ws + (item * kQT + qi) * D;
 #pragma unroll
-    for (int dt = 0; dt < ND; ++dt)
+    for (int dt = 0; dt < C::ND; ++dt)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int d0 = dt * 32 + 8 * j + 4 * half;
-        // D + 2 floats per query: 8-byte aligned, so store in pairs
-        *reinterpret_cast<float2*>(wp + d0) = make_float2(o[dt][4 * j], o[dt][4 * j + 1]);
-        *reinterpret_cast<float2*>(wp + d0 + 2) = make_float2(o[dt][4 * j + 2], o[dt][4 * j + 3]);
-      }
+      for (int j = 0; j < 4; ++j)
+        *reinterpret_cast<float4*>(wo + dt * 32 + 8 * j + 4 * half) =
+            make_float4(st.o[dt][4 * j], st.o[dt][4 * j + 1], st.o[dt][4 * j + 2],
+                        st.o[dt][4 * j + 3]);
     if (half == 0) {
-      wp[D] = m_run;
-      wp[D + 1] = l_run;
+      const int64_t n_items = (int64_t)gridDim.z * tile_slots * n_split_max;
+      float* ml = ws + n_items * kQT * D;
+      ml[(item * kQT + qi) * 2] = st.m_raw == -INFINITY ? -INFINITY : st.m_raw * c_log2;
+      ml[(item * kQT + qi) * 2 + 1] = l_run;
     }
   }
 }
 
-// Merge the split partials of every multi-split tile, in split order.
+// Merge the split partials of every multi-split tile, in split order.  One
+// thread per (query vector, 4 channels); consecutive threads read consecutive
+// 16-byte pieces of a partial.
 template <int D>
 __global__ void __launch_bounds__(256)
 combine_kernel(int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total,
@@ -363,46 +514,41 @@ combine_kernel(int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total,
   if (kend <= kstart) return;
   const int n_split = (int)((kend - kstart + split_len - 1) / split_len);
   if (n_split <= 1 || n_split > n_split_max) return;
-  const int qi = threadIdx.x >> 1;        // query vector within the tile
-  const int dh = (threadIdx.x & 1) * (D / 2);
-  const int wave = qi / kQW, nq = qi % kQW;
-  const int row_idx = tile.r_begin + wave * (kQW >> log2g) + (nq >> log2g);
-  if (row_idx >= tile.r_end) return;
-  const int64_t t = rws[row_idx];
-  if (t < kstart || t >= kend) return;
-  const int head = g * G + (nq & (G - 1));
+  const int64_t n_items = (int64_t)gridDim.y * tile_slots * n_split_max;
+  const float* ml = ws + n_items * kQT * D;
   const int64_t item0 = ((int64_t)lg * tile_slots + slot) * n_split_max;
-  float M = -INFINITY;
-  for (int s = 0; s < n_split; ++s) M = fmaxf(M, ws[((item0 + s) * kQT + qi) * (D + 2) + D]);
-  float Lsum = 0.0f;
-  float acc[D / 2];
-#pragma unroll
-  for (int d = 0; d < D / 2; ++d) acc[d] = 0.0f;
-  for (int s = 0; s < n_split; ++s) {
-    const float* wp = ws + ((item0 + s) * kQT + qi) * (D + 2);
-    const float m = wp[D];
-    const float w = (m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m - M);
-    Lsum += w * wp[D + 1];
-#pragma unroll
-    for (int d = 0; d < D / 2; ++d) acc[d] += w * wp[dh + d];
-  }
-  const float inv = Lsum > 0.0f ? 1.0f / Lsum : 0.0f;
-  const int64_t ob = (((int64_t)l * t_total + t) * Hq + head) * D + dh;
-  if (out_f32) {
-    float* op = reinterpret_cast<float*>(out) + ob;
-#pragma unroll
-    for (int d = 0; d < D / 2; d += 4)
-      *reinterpret_cast<float4*>(op + d) =
-          make_float4(acc[d] * inv, acc[d + 1] * inv, acc[d + 2] * inv, acc[d + 3] * inv);
-  } else {
-    uint16_t* op = reinterpret_cast<uint16_t*>(out) + ob;
-#pragma unroll
-    for (int d = 0; d < D / 2; d += 8)
-      *reinterpret_cast<uint4*>(op + d) =
-          make_uint4(pack_bf16x2(acc[d] * inv, acc[d + 1] * inv),
-                     pack_bf16x2(acc[d + 2] * inv, acc[d + 3] * inv),
-                     pack_bf16x2(acc[d + 4] * inv, acc[d + 5] * inv),
-                     pack_bf16x2(acc[d + 6] * inv, acc[d + 7] * inv));
+  constexpr int Q4 = D / 4;  // 4-channel pieces per query vector
+  for (int e = blockIdx.z * blockDim.x + threadIdx.x; e < kQT * Q4; e += gridDim.z * blockDim.x) {
+    const int qi = e / Q4, c4 = (e % Q4) * 4;
+    const int wave = qi / kQW, nq = qi % kQW;
+    const int row_idx = tile.r_begin + wave * (kQW >> log2g) + (nq >> log2g);
+    if (row_idx >= tile.r_end) continue;
+    const int64_t t = rws[row_idx];
+    if (t < kstart || t >= kend) continue;
+    const int head = g * G + (nq & (G - 1));
+    float M = -INFINITY;
+    for (int s = 0; s < n_split; ++s) M = fmaxf(M, ml[((item0 + s) * kQT + qi) * 2]);
+    float Lsum = 0.0f;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s = 0; s < n_split; ++s) {
+      const float m = ml[((item0 + s) * kQT + qi) * 2];
+      const float w = (m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m - M);
+      Lsum += w * ml[((item0 + s) * kQT + qi) * 2 + 1];
+      const float4 o = *reinterpret_cast<const float4*>(ws + ((item0 + s) * kQT + qi) * D + c4);
+      acc.x += w * o.x;
+      acc.y += w * o.y;
+      acc.z += w * o.z;
+      acc.w += w * o.w;
+    }
+    const float inv = Lsum > 0.0f ? 1.0f / Lsum : 0.0f;
+    const int64_t ob = (((int64_t)l * t_total + t) * Hq + head) * D + c4;
+    if (out_f32) {
+      *reinterpret_cast<float4*>(reinterpret_cast<float*>(out) + ob) =
+          make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
+    } else {
+      *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(out) + ob) =
+          make_uint2(pack_bf16x2(acc.x * inv, acc.y * inv), pack_bf16x2(acc.z * inv, acc.w * inv));
+    }
   }
 }
 
@@ -434,11 +580,15 @@ bool attn_plan(int n_layers, int n_q_heads, int n_kv_heads, int head_dim, int64_
   plan->split_len = split_len;
   plan->n_split_max = (max_seq_len + split_len - 1) / split_len;
   if (plan->n_split_max < 1) plan->n_split_max = 1;
-  plan->workspace = plan->n_split_max > 1
-                        ? (size_t)n_layers * n_kv_heads * plan->tile_slots * plan->n_split_max *
-                              kQT * (head_dim + 2) * sizeof(float)
-                        : 0;
-  (void)t_total;
+  const size_t v16 = (size_t)n_layers * n_kv_heads * (size_t)t_total * head_dim * 2;
+  plan->v16_offset = 0;
+  size_t parts = 0;
+  if (plan->n_split_max > 1) {
+    const size_t items = (size_t)n_layers * n_kv_heads * plan->tile_slots * plan->n_split_max;
+    parts = items * kQT * (head_dim + 2) * sizeof(float);
+  }
+  plan->parts_offset = ((v16 + 255) / 256) * 256;
+  plan->workspace = plan->parts_offset + parts;
   return true;
 }
 
@@ -457,21 +607,28 @@ hipError_t launch_sparse_attn(const AttnPlan& plan, int n_layers, int n_q_heads,
                          n_kv_heads, head_dim, t_total, n_seqs, rows, cu_rows, rows_per_layer,
                          max_rows, k_fresh, v_fresh, k_cache, v_cache);
   }
+  uint16_t* v16 = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(workspace) + plan.v16_offset);
+  float* parts = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + plan.parts_offset);
+  {
+    const int64_t n8 = (int64_t)n_layers * n_kv_heads * t_total * head_dim / 8;
+    int64_t blocks = (n8 + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    hipLaunchKernelGGL(v16_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n8, v_cache, v16);
+  }
   const int log2g = ilog2(n_q_heads / n_kv_heads);
-  const float scale_log2 = softmax_scale * 1.4426950408889634f;
+  const float c_log2 = softmax_scale * 1.4426950408889634f;
   const int out_f32 = out_dtype == KVB_F32;
   const dim3 grid(plan.tile_slots, plan.n_split_max, n_layers * n_kv_heads);
-  float* ws = reinterpret_cast<float*>(workspace);
 #define KVB_ATTN(D)                                                                              \
   hipLaunchKernelGGL(attn_kernel<D>, grid, dim3(kThreads), 0, s, n_q_heads, n_kv_heads, log2g,   \
                      t_total, cu_seqlens, n_seqs, rows, cu_rows, rows_per_layer,                 \
                      plan.rows_per_tile, plan.tile_slots, plan.split_len, plan.n_split_max, q,    \
-                     k_cache, v_cache, scale_log2, out_f32, out, ws)
+                     k_cache, v16, c_log2, out_f32, out, parts)
 #define KVB_COMBINE(D)                                                                           \
-  hipLaunchKernelGGL(combine_kernel<D>, dim3(plan.tile_slots, n_layers * n_kv_heads), dim3(256), \
-                     0, s, n_q_heads, n_kv_heads, log2g, t_total, cu_seqlens, n_seqs, rows,      \
-                     cu_rows, rows_per_layer, plan.rows_per_tile, plan.tile_slots,               \
-                     plan.split_len, plan.n_split_max, out_f32, out, ws)
+  hipLaunchKernelGGL(combine_kernel<D>, dim3(plan.tile_slots, n_layers * n_kv_heads, 4),         \
+                     dim3(256), 0, s, n_q_heads, n_kv_heads, log2g, t_total, cu_seqlens, n_seqs,  \
+                     rows, cu_rows, rows_per_layer, plan.rows_per_tile, plan.tile_slots,          \
+                     plan.split_len, plan.n_split_max, out_f32, out, parts)
   if (head_dim == 128) {
     KVB_ATTN(128);
     if (plan.n_split_max > 1) KVB_COMBINE(128);
