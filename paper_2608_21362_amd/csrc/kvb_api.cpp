@@ -297,8 +297,9 @@ size_t kvb_sparse_attn_workspace_bytes(int32_t n_layers, int32_t n_q_heads, int3
       head_dim <= 0 || t_total <= 0 || n_seqs <= 0 || max_seq_len <= 0 || max_rows < 0)
     return 0;
   kvb::AttnPlan plan;
-  kvb::attn_plan(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs, max_seq_len,
-                 max_rows, &plan);
+  if (!kvb::attn_plan(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs, max_seq_len,
+                      max_rows, &plan))
+    return 0;
   return plan.workspace;
 }
 
@@ -329,8 +330,9 @@ kvb_status kvb_sparse_attn(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_hea
   const void* tens[] = {q, k_fresh, v_fresh, k_cache, v_cache, out};
   for (const void* p : tens) REQUIRE(p != nullptr && aligned16(p), "null or misaligned tensor");
   kvb::AttnPlan plan;
-  kvb::attn_plan(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs, max_seq_len, max_rows,
-                 &plan);
+  if (!kvb::attn_plan(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs, max_seq_len,
+                      max_rows, &plan))
+    return fail(KVB_EUNSUPPORTED, "too many attention work items (layers x kv heads x tiles x splits)");
   REQUIRE(workspace_bytes >= plan.workspace, "workspace %zu bytes, need %zu", workspace_bytes,
           plan.workspace);
   if (plan.workspace) REQUIRE(workspace != nullptr && aligned16(workspace), "workspace NULL or misaligned");

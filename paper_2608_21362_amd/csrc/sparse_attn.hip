@@ -55,11 +55,19 @@ typedef __attribute__((ext_vector_type(2))) _Float16 f16x2;
 typedef __attribute__((ext_vector_type(2))) float f32x2;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
 
-constexpr int kWaves = 4;
+#ifndef KVB_ATTN_WAVES
+#define KVB_ATTN_WAVES 4
+#endif
+constexpr int kWaves = KVB_ATTN_WAVES;  // waves per workgroup (each owns 32 query vectors)
 constexpr int kThreads = 64 * kWaves;
 constexpr int kQW = 32;                 // query vectors per wave
 constexpr int kQT = kQW * kWaves;       // query vectors per workgroup
-constexpr int kKB = 64;                 // keys per block
+// Workgroups per CU the register allocator targets (compile-time tunable).
+#ifndef KVB_ATTN_WG_PER_CU
+#define KVB_ATTN_WG_PER_CU 2
+#endif
+constexpr int kKB = 32;                 // keys per block = one 32-row MFMA tile
+constexpr int kStages = 4;              // LDS ring depth (blocks in flight: 2 ahead)
 constexpr float kLazy = 8.0f;           // max growth (log2 units) tolerated before a rescale
 
 #define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
@@ -71,10 +79,9 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-// wait until this wave's LDS operations have completed
-__device__ __forceinline__ void wait_lgkmcnt0() {
-  __builtin_amdgcn_s_waitcnt((0xF) | (0x3 << 14) | (0x7 << 4) | (0x0 << 8));
-}
+// Keep the compiler from moving memory accesses across this point (the raw
+// s_barrier builtin is not a memory barrier for it); emits no instruction.
+__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
 
 // ---------------------------------------------------------------- patch ----
 __global__ void __launch_bounds__(256)
@@ -245,46 +252,102 @@ struct AttnState {
   float l_part;  // this lane's share of the running sum
 };
 
+// max / sum of x over lanes l and l ^ 32.  v_permlane32_swap exchanges the
+// upper half of its first operand with the lower half of its second, so with
+// both holding x, lane l ends with x[l] and x[l ^ 32] in its two registers.  It
+// is written as inline assembly: the compiler builtin, given the same value
+// twice, has been lowered to read both results from one register.
+__device__ __forceinline__ void swap_halves(float& a, float& b) {
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ float max_halves(float x) {
+  float a = x, b = x;
+  swap_halves(a, b);
+  return fmaxf(a, b);
+}
+__device__ __forceinline__ float sum_halves(float x) {
+  float a = x, b = x;
+  swap_halves(a, b);
+  return a + b;
+}
+
+// K operand of one 32-key block: lane (row n, half h) holds d = (D/2) h + 8 s + v
 template <int D>
-__device__ __forceinline__ void attend_block(const char* k_st, const char* v_st,
-                                             const bf16x8 (&qop)[AttnCfg<D>::NS],
-                                             AttnState<D>& st, float c_log2, bool full,
-                                             int kb, int t_q, int k_hi, int lane) {
+__device__ __forceinline__ void read_k(const char* k_st, int lane,
+                                       bf16x8 (&kr)[AttnCfg<D>::NS]) {
   using C = AttnCfg<D>;
   const int half = lane >> 5, n = lane & 31;
-  // S^T = K Q^T
-  f32x16 sacc[2];
+  const char* krow = k_st + n * C::ROWB;
 #pragma unroll
-  for (int kt = 0; kt < 2; ++kt) {
-    sacc[kt] = f32x16{};
-    const int r = kt * 32 + n;
-    const char* krow = k_st + r * C::ROWB;
-#pragma unroll
-    for (int s = 0; s < C::NS; ++s) {
-      const int chunk = (D / 16) * half + s;
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + 16 * (chunk ^ C::swz_k(r)));
-      sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qop[s], sacc[kt], 0, 0, 0);
-    }
+  for (int s = 0; s < C::NS; ++s) {
+    const int chunk = (D / 16) * half + s;
+    kr[s] = *reinterpret_cast<const bf16x8*>(krow + 16 * (chunk ^ C::swz_k(n)));
   }
-  if (!full) {
+}
+
+// V^T operands of one 32-key block, for 16-key step ks and 32-row d tile dt.
+// Transpose-read lane address: row 16 ks + 8 hh + 4 half + j/4, d = dbase + 4 (j % 4);
+// the two reads are joined as whole registers (keys 4h..4h+3, then 8+4h..8+4h+3:
+// element-wise 16-bit extraction here has been miscompiled into a broadcast).
+template <int D>
+__device__ __forceinline__ void read_v(const char* v_st, int lane,
+                                       f16x8 (&vr)[2][AttnCfg<D>::ND]) {
+  using C = AttnCfg<D>;
+  const int half = lane >> 5, j = lane & 15, grp = (lane >> 4) & 1;
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+  for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kb + kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        if (key > t_q || key >= k_hi) sacc[kt][r] = -INFINITY;
+    for (int dt = 0; dt < C::ND; ++dt) {
+      const int elem = dt * 32 + 16 * grp + 4 * (j & 3);
+      const int chunk = elem >> 3;
+      u32x2 part[2];
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int row = ks * 16 + 8 * hh + 4 * half + (j >> 2);
+        const char* addr = v_st + row * C::ROWB + 16 * (chunk ^ C::swz_v(row)) + 2 * (elem & 7);
+        part[hh] = __builtin_bit_cast(
+            u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, addr)));
       }
+      const u32x4 w = {part[0][0], part[0][1], part[1][0], part[1][1]};
+      vr[ks][dt] = __builtin_bit_cast(f16x8, w);
+    }
+}
+
+// S^T (32 keys x 32 queries) = K Q^T
+template <int D>
+__device__ __forceinline__ f32x16 scores(const bf16x8 (&kr)[AttnCfg<D>::NS],
+                                         const bf16x8 (&qop)[AttnCfg<D>::NS]) {
+  f32x16 acc = {};
+#pragma unroll
+  for (int s = 0; s < AttnCfg<D>::NS; ++s)
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kr[s], qop[s], acc, 0, 0, 0);
+  return acc;
+}
+
+// Online-softmax update for one block of scores: masks keys past the query
+// (or past the split), refreshes the running maximum when it grew by more than
+// kLazy, and returns the probabilities as the fp16 P^T operands of the two
+// 16-key steps (accumulator registers 0..7 and 8..15).
+template <int D>
+__device__ __forceinline__ void softmax_block(f32x16 sacc, AttnState<D>& st, float c_log2,
+                                              bool full, int kb, int t_q, int k_hi, int lane,
+                                              f16x8 (&pb)[2]) {
+  using C = AttnCfg<D>;
+  const int half = lane >> 5;
+  if (__builtin_expect(!full, 0)) {
+    // key kb + off is allowed iff off <= lim (off = 8(r/4) + 4 half + r%4)
+    const int lim = min(t_q, k_hi - 1) - kb - 4 * half;
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (8 * (r >> 2) + (r & 3) > lim) sacc[r] = -INFINITY;
   }
-  float bmax = sacc[0][0];
+  float bmax = sacc[0];
 #pragma unroll
-  for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) bmax = fmaxf(bmax, sacc[kt][r]);
-  bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
+  for (int r = 1; r < 16; ++r) bmax = fmaxf(bmax, sacc[r]);
+  bmax = max_halves(bmax);
   const float m_new = fmaxf(st.m_raw, bmax);
-  // refresh the reference maximum only when some lane's scores grew by > kLazy
   const bool grow = (m_new - st.m_raw) * c_log2 > kLazy || st.m_raw == -INFINITY;
-  if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+  if (__builtin_expect(__builtin_amdgcn_ballot_w64(grow) != 0, 0)) {
     const float alpha = (st.m_raw == -INFINITY || m_new == -INFINITY)
                             ? (m_new == -INFINITY ? 1.0f : 0.0f)
                             : __builtin_amdgcn_exp2f((st.m_raw - m_new) * c_log2);
@@ -296,70 +359,37 @@ __device__ __forceinline__ void attend_block(const char* k_st, const char* v_st,
     st.m_raw = m_new;
   }
   const float mc = st.m_raw == -INFINITY ? 0.0f : st.m_raw * c_log2;
-  float psum = 0.0f;
+  const f16x2 ones = {(_Float16)1.0f, (_Float16)1.0f};
+  float psum = st.l_part;
 #pragma unroll
-  for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][r], c_log2, -mc));
-      sacc[kt][r] = p;
-      psum += p;
-    }
-  st.l_part += psum;
-  // O^T += V^T P^T over four 16-key steps
-#pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    const int kt = ks >> 1, r0 = 8 * (ks & 1);
-    f16x8 pb;
+  for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
     for (int v = 0; v < 8; v += 2) {
-      const f32x2 f = {sacc[kt][r0 + v], sacc[kt][r0 + v + 1]};
-      const f16x2 h = __builtin_convertvector(f, f16x2);
-      pb[v] = h[0];
-      pb[v + 1] = h[1];
+      const f32x2 e = {__builtin_amdgcn_exp2f(__builtin_fmaf(sacc[8 * ks + v], c_log2, -mc)),
+                       __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[8 * ks + v + 1], c_log2, -mc))};
+      const f16x2 h = __builtin_convertvector(e, f16x2);
+      // the running sum adds the same fp16 values the P.V product uses
+      psum = __builtin_amdgcn_fdot2(h, ones, psum, false);
+      pb[ks][v] = h[0];
+      pb[ks][v + 1] = h[1];
     }
-    // transpose-read lane address: row kbase + j/4, d = dbase + 4 (j % 4)
-    const int j = lane & 15, grp = (lane >> 4) & 1;
-#pragma unroll
-    for (int dt = 0; dt < C::ND; ++dt) {
-      const int dbase = dt * 32 + 16 * grp;
-      u32x2 part[2];
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const int row = ks * 16 + 8 * hh + 4 * half + (j >> 2);
-        const int elem = dbase + 4 * (j & 3);
-        const int chunk = elem >> 3;
-        const char* addr = v_st + row * C::ROWB + 16 * (chunk ^ C::swz_v(row)) + 2 * (elem & 7);
-        part[hh] = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, addr)));
-      }
-      // whole-register concatenation (keys 4h..4h+3, then 8+4h..8+4h+3); element-wise
-      // 16-bit extraction here has been miscompiled into a broadcast of element 0
-      const u32x4 w = {part[0][0], part[0][1], part[1][0], part[1][1]};
-      const f16x8 a = __builtin_bit_cast(f16x8, w);
-      st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, pb, st.o[dt], 0, 0, 0);
-    }
-  }
+  st.l_part = psum;
 }
 
+// One work item: (layer, kv head, tile slot, KV split).  Returns without work
+// when the slot holds no tile or the tile has fewer splits.
 template <int D>
-__global__ void __launch_bounds__(kThreads, 2)
-attn_kernel(int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total,
-            const int32_t* __restrict__ cu_seqlens, int32_t n_seqs,
-            const int32_t* __restrict__ rows, const int32_t* __restrict__ cu_rows,
-            int32_t rows_per_layer, int32_t rows_per_tile, int32_t tile_slots, int32_t split_len,
-            int32_t n_split_max, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
-            const uint16_t* __restrict__ v16, float c_log2, int32_t out_f32,
-            void* __restrict__ out, float* __restrict__ ws) {
+__device__ __forceinline__ void attend_item(
+    int lg, int slot, int split, int n_lg, char* k_ring, char* v_ring,
+    int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total, const int32_t* __restrict__ cu_seqlens,
+    int32_t n_seqs, const int32_t* __restrict__ rows, const int32_t* __restrict__ cu_rows,
+    int32_t rows_per_layer, int32_t rows_per_tile, int32_t tile_slots, int32_t split_len,
+    int32_t n_split_max, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
+    const uint16_t* __restrict__ v16, float c_log2, int32_t out_f32, void* __restrict__ out,
+    float* __restrict__ ws) {
   using C = AttnCfg<D>;
-  __shared__ __attribute__((aligned(1024))) char k_st0[C::BLK];
-  __shared__ __attribute__((aligned(1024))) char k_st1[C::BLK];
-  __shared__ __attribute__((aligned(1024))) char v_st0[C::BLK];
-  __shared__ __attribute__((aligned(1024))) char v_st1[C::BLK];
-
   const int G = 1 << log2g;
-  const int lg = blockIdx.z;
   const int l = lg / Hkv, g = lg % Hkv;
-  const int slot = blockIdx.x, split = blockIdx.y;
   const int64_t set = rows_per_layer ? l : 0;
   const int32_t* cur = cu_rows + set * (n_seqs + 1);
   const int32_t* rws = rows + set * t_total;
@@ -390,8 +420,11 @@ attn_kernel(int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total,
   const i32x4 vrs = buffer_rsrc(v16 + kv_base, T * C::ROWB);
   const LoadOffsets<D> lo = load_offsets<D>(wave, lane);
   const int nblk = (k_hi - k_lo + kKB - 1) / kKB;
+  static_assert(kStages == 4, "stage index arithmetic assumes a 4-deep ring");
+  auto kst = [&](int b) { return k_ring + (b & 3) * C::BLK; };  // ring stage of block b
+  auto vst = [&](int b) { return v_ring + (b & 3) * C::BLK; };
 
-  issue_block<D>(krs, vrs, k_lo, lo, k_st0, v_st0, wave);
+  issue_block<D>(krs, vrs, k_lo, lo, kst(0), vst(0), wave);
 
   // Q^T operand: query n, d = (D/2) h + 8 s + v
   bf16x8 qop[C::NS];
@@ -404,10 +437,13 @@ attn_kernel(int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total,
       qop[s] = __builtin_bit_cast(bf16x8, w);
     }
   }
-  // Q (and the first block) must have landed before the loop: this keeps the
-  // compiler from waiting on the queries -- and so on the in-flight prefetch --
-  // inside the loop.
+  // Q and block 0 land before anything else is issued: the compiler then never
+  // waits on the queries -- and so on the in-flight prefetch -- later on.
   wait_vmcnt<0>();
+  if (nblk > 1) issue_block<D>(krs, vrs, k_lo + kKB, lo, kst(1), vst(1), wave);
+  if (nblk > 2) issue_block<D>(krs, vrs, k_lo + 2 * kKB, lo, kst(2), vst(2), wave);
+  __builtin_amdgcn_s_barrier();
+  compiler_fence();
 
   AttnState<D> st;
 #pragma unroll
@@ -415,41 +451,40 @@ attn_kernel(int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total,
   st.m_raw = -INFINITY;
   st.l_part = 0.0f;
 
-  for (int jb = 0; jb < nblk; jb += 2) {
-    // even block: stage 0 (next block goes to stage 1)
-    {
-      const int kb = k_lo + jb * kKB;
-      if (jb + 1 < nblk) {
-        issue_block<D>(krs, vrs, kb + kKB, lo, k_st1, v_st1, wave);
-        wait_vmcnt<2 * C::LOADS>();
-      } else {
-        wait_vmcnt<0>();
-      }
-      __builtin_amdgcn_s_barrier();
-      const bool full = (kb + kKB - 1 <= t_min) && (kb + kKB <= k_hi);
-      attend_block<D>(k_st0, v_st0, qop, st, c_log2, full, kb, t_q, k_hi, lane);
-      wait_lgkmcnt0();
-      __builtin_amdgcn_s_barrier();
-    }
-    if (jb + 1 < nblk) {
-      // odd block: stage 1 (next block goes to stage 0)
-      const int kb = k_lo + (jb + 1) * kKB;
-      if (jb + 2 < nblk) {
-        issue_block<D>(krs, vrs, kb + kKB, lo, k_st0, v_st0, wave);
-        wait_vmcnt<2 * C::LOADS>();
-      } else {
-        wait_vmcnt<0>();
-      }
-      __builtin_amdgcn_s_barrier();
-      const bool full = (kb + kKB - 1 <= t_min) && (kb + kKB <= k_hi);
-      attend_block<D>(k_st1, v_st1, qop, st, c_log2, full, kb, t_q, k_hi, lane);
-      wait_lgkmcnt0();
-      __builtin_amdgcn_s_barrier();
-    }
+  // Software pipeline over blocks: iteration j computes the scores of block
+  // j + 1 on the matrix cores while the vector units turn the scores of block j
+  // into probabilities, then accumulates P V for block j.  The ring holds
+  // blocks j .. j + 3; block j + 3 is requested once every wave has finished
+  // block j - 1 (the barrier), whose stage it reuses.
+  bf16x8 kr[C::NS];
+  read_k<D>(kst(0), lane, kr);
+  f32x16 sacc = scores<D>(kr, qop);
+  for (int j = 0; j < nblk; ++j) {
+    const int kb = k_lo + j * kKB;
+    if (j + 2 < nblk)
+      wait_vmcnt<2 * C::LOADS>();  // block j + 1 landed, block j + 2 may be in flight
+    else
+      wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    compiler_fence();
+    if (j + 3 < nblk) issue_block<D>(krs, vrs, kb + 3 * kKB, lo, kst(j + 3), vst(j + 3), wave);
+    // on the last iteration this reads a stale stage; those scores are never used
+    read_k<D>(kst(j + 1), lane, kr);
+    f16x8 vr[2][C::ND];
+    read_v<D>(vst(j), lane, vr);
+    const bool full = (kb + kKB - 1 <= t_min) && (kb + kKB <= k_hi);
+    f16x8 pb[2];
+    softmax_block<D>(sacc, st, c_log2, full, kb, t_q, k_hi, lane, pb);
+    sacc = scores<D>(kr, qop);
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int dt = 0; dt < C::ND; ++dt)
+        st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[ks][dt], pb[ks], st.o[dt], 0, 0, 0);
   }
 
   if (!qvalid) return;
-  const float l_run = st.l_part + __shfl_xor(st.l_part, 32, 64);
+  const float l_run = sum_halves(st.l_part);
   if (n_split == 1) {
     const float inv = (l_run > 0.0f) ? 1.0f / l_run : 0.0f;
     const int64_t ob = (((int64_t)l * t_total + t_q) * Hq + head) * D;
@@ -481,12 +516,34 @@ attn_kernel(int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total,
             make_float4(st.o[dt][4 * j], st.o[dt][4 * j + 1], st.o[dt][4 * j + 2],
                         st.o[dt][4 * j + 3]);
     if (half == 0) {
-      const int64_t n_items = (int64_t)gridDim.z * tile_slots * n_split_max;
+      const int64_t n_items = (int64_t)n_lg * tile_slots * n_split_max;
       float* ml = ws + n_items * kQT * D;
       ml[(item * kQT + qi) * 2] = st.m_raw == -INFINITY ? -INFINITY : st.m_raw * c_log2;
       ml[(item * kQT + qi) * 2 + 1] = l_run;
     }
   }
+}
+
+
+// Grid (tile slot, KV split, layer x kv head).  Workgroups whose slot holds no
+// tile, or whose tile has fewer splits, exit at once; the hardware dispatcher
+// hands their place to the next workgroup, so the grid load-balances itself.
+template <int D>
+__global__ void __launch_bounds__(kThreads, KVB_ATTN_WG_PER_CU)
+attn_kernel(int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total,
+            const int32_t* __restrict__ cu_seqlens, int32_t n_seqs,
+            const int32_t* __restrict__ rows, const int32_t* __restrict__ cu_rows,
+            int32_t rows_per_layer, int32_t rows_per_tile, int32_t tile_slots, int32_t split_len,
+            int32_t n_split_max, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
+            const uint16_t* __restrict__ v16, float c_log2, int32_t out_f32,
+            void* __restrict__ out, float* __restrict__ ws) {
+  using C = AttnCfg<D>;
+  __shared__ __attribute__((aligned(1024))) char k_ring[kStages * C::BLK];
+  __shared__ __attribute__((aligned(1024))) char v_ring[kStages * C::BLK];
+  attend_item<D>(blockIdx.z, blockIdx.x, blockIdx.y, gridDim.z, k_ring, v_ring, Hq,
+                 Hkv, log2g, t_total, cu_seqlens, n_seqs, rows, cu_rows, rows_per_layer,
+                 rows_per_tile, tile_slots, split_len, n_split_max, q, kc, v16, c_log2, out_f32,
+                 out, ws);
 }
 
 // Merge the split partials of every multi-split tile, in split order.  One
@@ -526,19 +583,48 @@ combine_kernel(int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total,
     const int64_t t = rws[row_idx];
     if (t < kstart || t >= kend) continue;
     const int head = g * G + (nq & (G - 1));
-    float M = -INFINITY;
-    for (int s = 0; s < n_split; ++s) M = fmaxf(M, ml[((item0 + s) * kQT + qi) * 2]);
-    float Lsum = 0.0f;
+    // splits are taken 8 at a time with every load of a group issued before
+    // any is used; groups are merged with the usual running-maximum rescale
+    constexpr int U = 8;
+    float M = -INFINITY, Lsum = 0.0f;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int s = 0; s < n_split; ++s) {
-      const float m = ml[((item0 + s) * kQT + qi) * 2];
-      const float w = (m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m - M);
-      Lsum += w * ml[((item0 + s) * kQT + qi) * 2 + 1];
-      const float4 o = *reinterpret_cast<const float4*>(ws + ((item0 + s) * kQT + qi) * D + c4);
-      acc.x += w * o.x;
-      acc.y += w * o.y;
-      acc.z += w * o.z;
-      acc.w += w * o.w;
+    for (int s0 = 0; s0 < n_split; s0 += U) {
+      float m[U], ls[U];
+      float4 o[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (s0 + u < n_split) {
+          const int64_t it = (item0 + s0 + u) * kQT + qi;
+          const float2 v = *reinterpret_cast<const float2*>(ml + it * 2);
+          m[u] = v.x;
+          ls[u] = v.y;
+          o[u] = *reinterpret_cast<const float4*>(ws + it * D + c4);
+        } else {
+          m[u] = -INFINITY;
+          ls[u] = 0.0f;
+          o[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+      float Mn = M;
+#pragma unroll
+      for (int u = 0; u < U; ++u) Mn = fmaxf(Mn, m[u]);
+      if (Mn == -INFINITY) continue;
+      const float a = (M == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(M - Mn);
+      Lsum *= a;
+      acc.x *= a;
+      acc.y *= a;
+      acc.z *= a;
+      acc.w *= a;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const float w = (m[u] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m[u] - Mn);
+        Lsum += w * ls[u];
+        acc.x += w * o[u].x;
+        acc.y += w * o[u].y;
+        acc.z += w * o[u].z;
+        acc.w += w * o[u].w;
+      }
+      M = Mn;
     }
     const float inv = Lsum > 0.0f ? 1.0f / Lsum : 0.0f;
     const int64_t ob = (((int64_t)l * t_total + t) * Hq + head) * D + c4;
@@ -587,6 +673,8 @@ bool attn_plan(int n_layers, int n_q_heads, int n_kv_heads, int head_dim, int64_
     const size_t items = (size_t)n_layers * n_kv_heads * plan->tile_slots * plan->n_split_max;
     parts = items * kQT * (head_dim + 2) * sizeof(float);
   }
+  const int64_t n_items = (int64_t)n_layers * n_kv_heads * plan->tile_slots * plan->n_split_max;
+  if (n_items > INT32_MAX) return false;
   plan->parts_offset = ((v16 + 255) / 256) * 256;
   plan->workspace = plan->parts_offset + parts;
   return true;
