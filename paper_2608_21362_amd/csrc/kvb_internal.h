@@ -42,10 +42,12 @@ hipError_t launch_select(int32_t n_sets, int64_t t_total, const int32_t* cu_seql
 struct AttnPlan {
   int rows_per_tile;   // selected rows per workgroup tile
   int tile_slots;      // tile slots per (layer, kv head)
-  int split_len;       // keys per split (multiple of the key block)
-  int n_split_max;     // splits per tile slot
+  int n_tiles;         // layers x kv heads x tile slots
+  int n_wg_max;        // most attention workgroups a launch uses
+  int n_rec;           // partial records (two per workgroup)
   size_t v16_offset;   // workspace offset of the fp16 copy of V
-  size_t parts_offset; // workspace offset of the split partials
+  size_t plan_offset;  // workspace offset of the work decomposition (int32)
+  size_t parts_offset; // workspace offset of the partial records
   size_t workspace;    // total workspace bytes
 };
 bool attn_plan(int n_layers, int n_q_heads, int n_kv_heads, int head_dim, int64_t t_total,

@@ -68,6 +68,7 @@ constexpr int kQT = kQW * kWaves;       // query vectors per workgroup
 #endif
 constexpr int kKB = 32;                 // keys per block = one 32-row MFMA tile
 constexpr int kStages = 4;              // LDS ring depth (blocks in flight: 2 ahead)
+constexpr int kAttnMaxWorkgroups = 1024;  // attention workgroups (sizes the partial records)
 constexpr float kLazy = 8.0f;           // max growth (log2 units) tolerated before a rescale
 
 #define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
@@ -77,6 +78,11 @@ template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// wait until this wave's LDS operations have completed
+__device__ __forceinline__ void wait_lgkmcnt0() {
+  __builtin_amdgcn_s_waitcnt((0xF) | (0x3 << 14) | (0x7 << 4) | (0x0 << 8));
 }
 
 // Keep the compiler from moving memory accesses across this point (the raw
@@ -376,17 +382,26 @@ __device__ __forceinline__ void softmax_block(f32x16 sacc, AttnState<D>& st, flo
   st.l_part = psum;
 }
 
-// One work item: (layer, kv head, tile slot, KV split).  Returns without work
-// when the slot holds no tile or the tile has fewer splits.
+// Partial records: n_rec x kQT x D fp16 normalised outputs, then n_rec x kQT
+// (max, sum) float pairs at this byte offset.
 template <int D>
-__device__ __forceinline__ void attend_item(
-    int lg, int slot, int split, int n_lg, char* k_ring, char* v_ring,
+__host__ __device__ constexpr int64_t rec_ml_offset(int64_t n_rec) {
+  return ((n_rec * kQT * D * 2 + 255) / 256) * 256;
+}
+
+// One segment: key blocks [blk_lo, blk_hi) (32 keys each, counted from the
+// tile's prompt start) of one tile of selected rows of (layer, kv head).  With
+// rec < 0 the segment covers the whole tile and writes the normalised output;
+// otherwise it writes partial record `rec` (unnormalised O, running maximum in
+// log2 units, running sum) for the combine pass.
+template <int D>
+__device__ __forceinline__ void attend_segment(
+    int lg, int slot, int blk_lo, int blk_hi, int rec, int n_rec, char* k_ring, char* v_ring,
     int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total, const int32_t* __restrict__ cu_seqlens,
     int32_t n_seqs, const int32_t* __restrict__ rows, const int32_t* __restrict__ cu_rows,
-    int32_t rows_per_layer, int32_t rows_per_tile, int32_t tile_slots, int32_t split_len,
-    int32_t n_split_max, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
-    const uint16_t* __restrict__ v16, float c_log2, int32_t out_f32, void* __restrict__ out,
-    float* __restrict__ ws) {
+    int32_t rows_per_layer, int32_t rows_per_tile, const uint16_t* __restrict__ q,
+    const uint16_t* __restrict__ kc, const uint16_t* __restrict__ v16, float c_log2,
+    int32_t out_f32, void* __restrict__ out, float* __restrict__ parts) {
   using C = AttnCfg<D>;
   const int G = 1 << log2g;
   const int l = lg / Hkv, g = lg % Hkv;
@@ -398,12 +413,15 @@ __device__ __forceinline__ void attend_item(
   const int T = (int)t_total;
   const int kstart = cu_seqlens[tile.b];
   const int kend = min(rws[tile.r_end - 1] + 1, T);
-  if (kend <= kstart) return;
-  const int n_split = (kend - kstart + split_len - 1) / split_len;
-  if (split >= n_split || n_split > n_split_max) return;
-  const int k_lo = kstart + split * split_len;
-  const int k_hi = min(k_lo + split_len, kend);
+  const int k_lo = kstart + blk_lo * kKB;
+  const int k_hi = min(kstart + blk_hi * kKB, kend);
+  if (k_hi <= k_lo) return;
   const int t_min = rws[tile.r_begin];
+
+  // the previous segment of this workgroup is done with the LDS ring
+  wait_lgkmcnt0();
+  __builtin_amdgcn_s_barrier();
+  compiler_fence();
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -485,7 +503,7 @@ __device__ __forceinline__ void attend_item(
 
   if (!qvalid) return;
   const float l_run = sum_halves(st.l_part);
-  if (n_split == 1) {
+  if (rec < 0) {
     const float inv = (l_run > 0.0f) ? 1.0f / l_run : 0.0f;
     const int64_t ob = (((int64_t)l * t_total + t_q) * Hq + head) * D;
 #pragma unroll
@@ -504,138 +522,258 @@ __device__ __forceinline__ void attend_item(
         }
       }
   } else {
-    // partial (unnormalised O, running max in log2 units, sum) of this split
-    const int64_t item = ((int64_t)lg * tile_slots + slot) * n_split_max + split;
+    // partial record: O normalised by this segment's own sum, in fp16 (|O| is
+    // bounded by max |V|, which fits fp16), plus (running max in log2 units, sum)
     const int qi = wave * kQW + n;
-    float* wo = ws + (item * kQT + qi) * D;
+    const float inv = (l_run > 0.0f) ? 1.0f / l_run : 0.0f;
+    uint16_t* wo = reinterpret_cast<uint16_t*>(parts) + ((int64_t)rec * kQT + qi) * D;
 #pragma unroll
     for (int dt = 0; dt < C::ND; ++dt)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        *reinterpret_cast<float4*>(wo + dt * 32 + 8 * j + 4 * half) =
-            make_float4(st.o[dt][4 * j], st.o[dt][4 * j + 1], st.o[dt][4 * j + 2],
-                        st.o[dt][4 * j + 3]);
+      for (int j = 0; j < 4; ++j) {
+        const f32x2 lo2 = {st.o[dt][4 * j] * inv, st.o[dt][4 * j + 1] * inv};
+        const f32x2 hi2 = {st.o[dt][4 * j + 2] * inv, st.o[dt][4 * j + 3] * inv};
+        const u32x2 h = {__builtin_bit_cast(unsigned, __builtin_convertvector(lo2, f16x2)),
+                         __builtin_bit_cast(unsigned, __builtin_convertvector(hi2, f16x2))};
+        *reinterpret_cast<u32x2*>(wo + dt * 32 + 8 * j + 4 * half) = h;
+      }
     if (half == 0) {
-      const int64_t n_items = (int64_t)n_lg * tile_slots * n_split_max;
-      float* ml = ws + n_items * kQT * D;
-      ml[(item * kQT + qi) * 2] = st.m_raw == -INFINITY ? -INFINITY : st.m_raw * c_log2;
-      ml[(item * kQT + qi) * 2 + 1] = l_run;
+      float* ml = reinterpret_cast<float*>(reinterpret_cast<char*>(parts) + rec_ml_offset<D>(n_rec)) +
+                  ((int64_t)rec * kQT + qi) * 2;
+      *reinterpret_cast<float2*>(ml) =
+          make_float2(st.m_raw == -INFINITY ? -INFINITY : st.m_raw * c_log2, l_run);
     }
   }
 }
 
+// int32 offset of the per-tile metadata inside the plan area
+__host__ __device__ constexpr int64_t tile_meta_offset(int64_t n_tiles, int64_t n_wg_max) {
+  return ((3 + n_tiles + n_wg_max + 3) / 4) * 4;
+}
 
-// Grid (tile slot, KV split, layer x kv head).  Workgroups whose slot holds no
-// tile, or whose tile has fewer splits, exit at once; the hardware dispatcher
-// hands their place to the next workgroup, so the grid load-balances itself.
-template <int D>
-__global__ void __launch_bounds__(kThreads, KVB_ATTN_WG_PER_CU)
-attn_kernel(int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total,
+// Work decomposition.  Work unit = one 32-key block of one tile; units are
+// numbered tile by tile (tile index = (layer x kv head) * tile_slots + slot).
+// One workgroup builds the exclusive prefix sum of the tiles' block counts,
+// then every attention workgroup w takes the contiguous units [w C, (w+1) C)
+// with C = ceil(total / n_wg), so all workgroups get the same work.
+//   plan[0] = C, plan[1] = total, plan[2 .. 2+n_tiles] = prefix,
+//   plan[3+n_tiles .. 3+n_tiles+n_wg) = tile holding unit w C,
+//   then per tile an int4 {first row entry, end row entry, key start, key end}
+//   at the 16-byte aligned offset tile_meta_offset(n_tiles, n_wg_max).
+__global__ void __launch_bounds__(1024)
+plan_kernel(int32_t n_tiles, int32_t tile_slots, int32_t Hkv, int64_t t_total,
             const int32_t* __restrict__ cu_seqlens, int32_t n_seqs,
             const int32_t* __restrict__ rows, const int32_t* __restrict__ cu_rows,
-            int32_t rows_per_layer, int32_t rows_per_tile, int32_t tile_slots, int32_t split_len,
-            int32_t n_split_max, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
-            const uint16_t* __restrict__ v16, float c_log2, int32_t out_f32,
-            void* __restrict__ out, float* __restrict__ ws) {
+            int32_t rows_per_layer, int32_t rows_per_tile, int32_t n_wg, int32_t n_wg_max,
+            int32_t* __restrict__ plan) {
+  int4* meta = reinterpret_cast<int4*>(plan + tile_meta_offset(n_tiles, n_wg_max));
+  __shared__ int warp_sums[16];
+  __shared__ int carry_sh;
+  int32_t* prefix = plan + 2;
+  int32_t* first = plan + 3 + n_tiles;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  if (tid == 0) carry_sh = 0;
+  __syncthreads();
+  for (int base = 0; base < n_tiles; base += 1024) {
+    const int t = base + tid;
+    int nb = 0;
+    if (t < n_tiles) {
+      const int lg = t / tile_slots, slot = t % tile_slots;
+      const int64_t set = rows_per_layer ? lg / Hkv : 0;
+      const int32_t* cur = cu_rows + set * (n_seqs + 1);
+      Tile tile;
+      int4 mt = make_int4(0, 0, 0, 0);
+      if (find_tile(cur, n_seqs, rows_per_tile, slot, &tile)) {
+        const int64_t kstart = cu_seqlens[tile.b];
+        const int64_t kend = min((int64_t)rows[set * t_total + tile.r_end - 1] + 1, t_total);
+        if (kend > kstart) nb = (int)((kend - kstart + kKB - 1) / kKB);
+        mt = make_int4(tile.r_begin, tile.r_end, (int)kstart, (int)kend);
+      }
+      meta[t] = mt;
+    }
+    // inclusive scan over the 1024 threads: within each wave, then over waves
+    int x = nb;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, 64);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) warp_sums[wv] = x;
+    __syncthreads();
+    int before = carry_sh;
+    for (int i = 0; i < wv; ++i) before += warp_sums[i];
+    if (t < n_tiles) prefix[t] = before + x - nb;
+    __syncthreads();
+    if (tid == 1023) carry_sh = before + x;
+    __syncthreads();
+  }
+  const int total = carry_sh;
+  const int chunk = max(1, (total + n_wg - 1) / n_wg);
+  if (tid == 0) {
+    plan[0] = chunk;
+    plan[1] = total;
+    prefix[n_tiles] = total;
+  }
+  __syncthreads();
+  // tile holding unit w * chunk: the last t with prefix[t] <= w * chunk and a
+  // non-empty range
+  for (int w = tid; w < n_wg; w += 1024) {
+    const int u = w * chunk;
+    int lo = 0, hi = n_tiles - 1;  // find the largest t with prefix[t] <= u
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (prefix[mid] <= u) lo = mid; else hi = mid - 1;
+    }
+    first[w] = lo;
+  }
+}
+
+// Two launch shapes:
+//  * whole tiles (many tiles): workgroup t finishes tile t;
+//  * balanced ranges (few tiles): workgroup w walks the tiles that overlap its
+//    units [w C, (w+1) C); tiles covered whole are finished here, the cut ones
+//    (at most its first and its last) leave partial records 2w and 2w + 1.
+template <int D>
+__global__ void __launch_bounds__(kThreads, KVB_ATTN_WG_PER_CU)
+attn_kernel(int32_t balanced, int32_t n_tiles, int32_t Hq, int32_t Hkv, int32_t log2g,
+            int64_t t_total, const int32_t* __restrict__ cu_seqlens, int32_t n_seqs,
+            const int32_t* __restrict__ rows, const int32_t* __restrict__ cu_rows,
+            int32_t rows_per_layer, int32_t rows_per_tile, int32_t tile_slots,
+            const int32_t* __restrict__ plan, int32_t n_rec, const uint16_t* __restrict__ q,
+            const uint16_t* __restrict__ kc, const uint16_t* __restrict__ v16, float c_log2,
+            int32_t out_f32, void* __restrict__ out, float* __restrict__ parts) {
   using C = AttnCfg<D>;
   __shared__ __attribute__((aligned(1024))) char k_ring[kStages * C::BLK];
   __shared__ __attribute__((aligned(1024))) char v_ring[kStages * C::BLK];
-  attend_item<D>(blockIdx.z, blockIdx.x, blockIdx.y, gridDim.z, k_ring, v_ring, Hq,
-                 Hkv, log2g, t_total, cu_seqlens, n_seqs, rows, cu_rows, rows_per_layer,
-                 rows_per_tile, tile_slots, split_len, n_split_max, q, kc, v16, c_log2, out_f32,
-                 out, ws);
+  if (!balanced) {
+    const int t = blockIdx.x;
+    const int whole = (int)((t_total + kKB - 1) / kKB) + 1;
+    attend_segment<D>(t / tile_slots, t % tile_slots, 0, whole, -1, n_rec, k_ring, v_ring, Hq,
+                      Hkv, log2g, t_total, cu_seqlens, n_seqs, rows, cu_rows, rows_per_layer,
+                      rows_per_tile, q, kc, v16, c_log2, out_f32, out, parts);
+    return;
+  }
+  const int w = blockIdx.x;
+  const int chunk = plan[0], total = plan[1];
+  const int32_t* prefix = plan + 2;
+  int u = w * chunk;
+  const int u_end = min(u + chunk, total);
+  int t = plan[3 + n_tiles + w];
+  for (int seg = 0; u < u_end && t < n_tiles; ++t) {
+    const int p0 = prefix[t], p1 = prefix[t + 1];
+    if (p1 <= u) continue;  // empty tile (or before the range)
+    const int e = min(u_end, p1);
+    const int rec = (u == p0 && p1 <= u_end) ? -1 : 2 * w + (seg == 0 ? 0 : 1);
+    attend_segment<D>(t / tile_slots, t % tile_slots, u - p0, e - p0, rec, n_rec, k_ring, v_ring,
+                      Hq, Hkv, log2g, t_total, cu_seqlens, n_seqs, rows, cu_rows, rows_per_layer,
+                      rows_per_tile, q, kc, v16, c_log2, out_f32, out, parts);
+    u = e;
+    ++seg;
+  }
 }
 
-// Merge the split partials of every multi-split tile, in split order.  One
-// thread per (query vector, 4 channels); consecutive threads read consecutive
-// 16-byte pieces of a partial.
+// Merge the partial records of every tile that was cut between workgroups, in
+// key order.  One thread per (query vector, 8 channels).  Every load a thread
+// needs depends only on the plan: the records are requested together with the
+// query's row.
 template <int D>
 __global__ void __launch_bounds__(256)
-combine_kernel(int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total,
-               const int32_t* __restrict__ cu_seqlens, int32_t n_seqs,
-               const int32_t* __restrict__ rows, const int32_t* __restrict__ cu_rows,
-               int32_t rows_per_layer, int32_t rows_per_tile, int32_t tile_slots,
-               int32_t split_len, int32_t n_split_max, int32_t out_f32, void* __restrict__ out,
-               const float* __restrict__ ws) {
-  const int G = 1 << log2g;
-  const int lg = blockIdx.y;
+combine_kernel(int32_t n_tiles, int32_t n_wg_max, int32_t Hq, int32_t Hkv, int32_t log2g,
+               int64_t t_total, const int32_t* __restrict__ rows, int32_t rows_per_layer,
+               int32_t tile_slots, const int32_t* __restrict__ plan, int32_t n_rec,
+               int32_t out_f32, void* __restrict__ out, const float* __restrict__ parts) {
+  const int t = blockIdx.x;
+  const int chunk = plan[0];
+  const int p0 = plan[2 + t], p1 = plan[3 + t];
+  const int4 mt = reinterpret_cast<const int4*>(plan + tile_meta_offset(n_tiles, n_wg_max))[t];
+  if (p1 <= p0) return;
+  const int w_a = p0 / chunk, w_b = (p1 - 1) / chunk;
+  if (w_a == w_b) return;  // finished by one workgroup
+  constexpr int Q8 = D / 8;  // 8-channel pieces per query vector
+  const int e = blockIdx.y * blockDim.x + threadIdx.x;
+  if (e >= kQT * Q8) return;
+  const int qi = e / Q8, c8 = (e % Q8) * 8;
+  const int lg = t / tile_slots;
   const int l = lg / Hkv, g = lg % Hkv;
-  const int slot = blockIdx.x;
+  const int wave = qi / kQW, nq = qi % kQW;
+  const int row_idx = mt.x + wave * (kQW >> log2g) + (nq >> log2g);
+  if (row_idx >= mt.y) return;
   const int64_t set = rows_per_layer ? l : 0;
-  const int32_t* cur = cu_rows + set * (n_seqs + 1);
-  const int32_t* rws = rows + set * t_total;
-  Tile tile;
-  if (!find_tile(cur, n_seqs, rows_per_tile, slot, &tile)) return;
-  const int64_t kstart = cu_seqlens[tile.b];
-  const int64_t kend = min((int64_t)rws[tile.r_end - 1] + 1, t_total);
-  if (kend <= kstart) return;
-  const int n_split = (int)((kend - kstart + split_len - 1) / split_len);
-  if (n_split <= 1 || n_split > n_split_max) return;
-  const int64_t n_items = (int64_t)gridDim.y * tile_slots * n_split_max;
-  const float* ml = ws + n_items * kQT * D;
-  const int64_t item0 = ((int64_t)lg * tile_slots + slot) * n_split_max;
-  constexpr int Q4 = D / 4;  // 4-channel pieces per query vector
-  for (int e = blockIdx.z * blockDim.x + threadIdx.x; e < kQT * Q4; e += gridDim.z * blockDim.x) {
-    const int qi = e / Q4, c4 = (e % Q4) * 4;
-    const int wave = qi / kQW, nq = qi % kQW;
-    const int row_idx = tile.r_begin + wave * (kQW >> log2g) + (nq >> log2g);
-    if (row_idx >= tile.r_end) continue;
-    const int64_t t = rws[row_idx];
-    if (t < kstart || t >= kend) continue;
-    const int head = g * G + (nq & (G - 1));
-    // splits are taken 8 at a time with every load of a group issued before
-    // any is used; groups are merged with the usual running-maximum rescale
-    constexpr int U = 8;
-    float M = -INFINITY, Lsum = 0.0f;
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int s0 = 0; s0 < n_split; s0 += U) {
-      float m[U], ls[U];
-      float4 o[U];
+  const int tq = rows[set * t_total + row_idx];
+  // the tile is the first segment of every workgroup after w_a, and of w_a
+  // only if w_a's range starts exactly at the tile
+  const int rec_a = 2 * w_a + (w_a * chunk < p0 ? 1 : 0);
+  const int n_parts = w_b - w_a + 1;
+  const uint16_t* o16 = reinterpret_cast<const uint16_t*>(parts);
+  const float* ml = reinterpret_cast<const float*>(reinterpret_cast<const char*>(parts) +
+                                                   rec_ml_offset<D>(n_rec));
+  // records are taken 8 at a time, all loads of a group issued before any is
+  // used (indices past the last record repeat it with weight zero); groups are
+  // merged with the usual running-maximum rescale
+  constexpr int U = 8;
+  float M = -INFINITY, Lsum = 0.0f;
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0; s0 < n_parts; s0 += U) {
+    float m[U], ls[U];
+    u32x4 o[U];
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        if (s0 + u < n_split) {
-          const int64_t it = (item0 + s0 + u) * kQT + qi;
-          const float2 v = *reinterpret_cast<const float2*>(ml + it * 2);
-          m[u] = v.x;
-          ls[u] = v.y;
-          o[u] = *reinterpret_cast<const float4*>(ws + it * D + c4);
-        } else {
-          m[u] = -INFINITY;
-          ls[u] = 0.0f;
-          o[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-      }
-      float Mn = M;
-#pragma unroll
-      for (int u = 0; u < U; ++u) Mn = fmaxf(Mn, m[u]);
-      if (Mn == -INFINITY) continue;
-      const float a = (M == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(M - Mn);
-      Lsum *= a;
-      acc.x *= a;
-      acc.y *= a;
-      acc.z *= a;
-      acc.w *= a;
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const float w = (m[u] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m[u] - Mn);
-        Lsum += w * ls[u];
-        acc.x += w * o[u].x;
-        acc.y += w * o[u].y;
-        acc.z += w * o[u].z;
-        acc.w += w * o[u].w;
-      }
-      M = Mn;
+    for (int u = 0; u < U; ++u) {
+      const int i = min(s0 + u, n_parts - 1);
+      const int rec = (i == 0) ? rec_a : 2 * (w_a + i);
+      const int64_t it = (int64_t)rec * kQT + qi;
+      const float2 v = *reinterpret_cast<const float2*>(ml + it * 2);
+      m[u] = (s0 + u < n_parts) ? v.x : -INFINITY;
+      ls[u] = v.y;
+      o[u] = *reinterpret_cast<const u32x4*>(o16 + it * D + c8);
     }
-    const float inv = Lsum > 0.0f ? 1.0f / Lsum : 0.0f;
-    const int64_t ob = (((int64_t)l * t_total + t) * Hq + head) * D + c4;
-    if (out_f32) {
-      *reinterpret_cast<float4*>(reinterpret_cast<float*>(out) + ob) =
-          make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
-    } else {
-      *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(out) + ob) =
-          make_uint2(pack_bf16x2(acc.x * inv, acc.y * inv), pack_bf16x2(acc.z * inv, acc.w * inv));
+    float Mn = M;
+#pragma unroll
+    for (int u = 0; u < U; ++u) Mn = fmaxf(Mn, m[u]);
+    if (Mn == -INFINITY) continue;
+    const float a = (M == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(M - Mn);
+    Lsum *= a;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[c] *= a;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      // weight of a record = its sum rescaled to the common maximum (its O is
+      // already divided by its own sum)
+      const float wgt = (m[u] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m[u] - Mn) * ls[u];
+      Lsum += wgt;
+      const f16x8 h = __builtin_bit_cast(f16x8, o[u]);
+#pragma unroll
+      for (int c = 0; c < 8; ++c) acc[c] += wgt * (float)h[c];
     }
+    M = Mn;
   }
+  if (tq < mt.z || tq >= mt.w) return;  // not a query of this prompt
+  const int head = g * (1 << log2g) + (nq & ((1 << log2g) - 1));
+  const float inv = Lsum > 0.0f ? 1.0f / Lsum : 0.0f;
+  const int64_t ob = (((int64_t)l * t_total + tq) * Hq + head) * D + c8;
+  if (out_f32) {
+    float* op = reinterpret_cast<float*>(out) + ob;
+    *reinterpret_cast<float4*>(op) = make_float4(acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
+    *reinterpret_cast<float4*>(op + 4) = make_float4(acc[4] * inv, acc[5] * inv, acc[6] * inv, acc[7] * inv);
+  } else {
+    *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(out) + ob) =
+        make_uint4(pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv),
+                   pack_bf16x2(acc[4] * inv, acc[5] * inv), pack_bf16x2(acc[6] * inv, acc[7] * inv));
+  }
+}
+
+// Workgroups of the attention kernel the current device holds at once.
+int resident_workgroups() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (cached[dev] == 0) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+      cus = 256;
+    cached[dev] = cus * KVB_ATTN_WG_PER_CU;
+  }
+  return cached[dev];
 }
 
 int ilog2(int x) {
@@ -650,33 +788,27 @@ bool attn_plan(int n_layers, int n_q_heads, int n_kv_heads, int head_dim, int64_
                int n_seqs, int max_seq_len, int max_rows, AttnPlan* plan) {
   const int G = n_q_heads / n_kv_heads;
   const int rows_per_tile = kQT / G;
-  const int full_tiles = (max_rows + rows_per_tile - 1) / rows_per_tile;
+  const int64_t full_tiles = ((int64_t)max_rows + rows_per_tile - 1) / rows_per_tile;
+  const int64_t tile_slots = full_tiles + n_seqs;
+  const int64_t n_tiles = (int64_t)n_layers * n_kv_heads * tile_slots;
+  // block units must fit int32: at most n_tiles * ceil(max_seq_len / 32)
+  if (n_tiles * ((max_seq_len + kKB - 1) / kKB) > INT32_MAX / 2) return false;
   plan->rows_per_tile = rows_per_tile;
-  plan->tile_slots = full_tiles + n_seqs;
-  // enough workgroups to fill 256 CUs a few times over; never split below 1024 keys
-  const int64_t est = (int64_t)n_layers * n_kv_heads * (full_tiles > 0 ? full_tiles : 1);
-  int want = (int)((1024 + est - 1) / est);
-  int split_len = max_seq_len;
-  if (want > 1) {
-    split_len = (max_seq_len + want - 1) / want;
-    if (split_len < 1024) split_len = 1024;
-  }
-  split_len = ((split_len + kKB - 1) / kKB) * kKB;
-  if (split_len < kKB) split_len = kKB;
-  plan->split_len = split_len;
-  plan->n_split_max = (max_seq_len + split_len - 1) / split_len;
-  if (plan->n_split_max < 1) plan->n_split_max = 1;
+  plan->tile_slots = (int)tile_slots;
+  plan->n_tiles = (int)n_tiles;
+  plan->n_wg_max = kAttnMaxWorkgroups;
+  plan->n_rec = 2 * kAttnMaxWorkgroups;
   const size_t v16 = (size_t)n_layers * n_kv_heads * (size_t)t_total * head_dim * 2;
+  const size_t plan_ints = (size_t)tile_meta_offset(n_tiles, plan->n_wg_max) + 4 * (size_t)n_tiles;
+  const size_t parts = (size_t)(head_dim == 128 ? rec_ml_offset<128>(plan->n_rec)
+                                                 : rec_ml_offset<64>(plan->n_rec)) +
+                       (size_t)plan->n_rec * kQT * 2 * sizeof(float);
+  auto up = [](size_t x) { return ((x + 255) / 256) * 256; };
   plan->v16_offset = 0;
-  size_t parts = 0;
-  if (plan->n_split_max > 1) {
-    const size_t items = (size_t)n_layers * n_kv_heads * plan->tile_slots * plan->n_split_max;
-    parts = items * kQT * (head_dim + 2) * sizeof(float);
-  }
-  const int64_t n_items = (int64_t)n_layers * n_kv_heads * plan->tile_slots * plan->n_split_max;
-  if (n_items > INT32_MAX) return false;
-  plan->parts_offset = ((v16 + 255) / 256) * 256;
+  plan->plan_offset = up(v16);
+  plan->parts_offset = up(plan->plan_offset + plan_ints * sizeof(int32_t));
   plan->workspace = plan->parts_offset + parts;
+  (void)max_seq_len;
   return true;
 }
 
@@ -695,38 +827,47 @@ hipError_t launch_sparse_attn(const AttnPlan& plan, int n_layers, int n_q_heads,
                          n_kv_heads, head_dim, t_total, n_seqs, rows, cu_rows, rows_per_layer,
                          max_rows, k_fresh, v_fresh, k_cache, v_cache);
   }
-  uint16_t* v16 = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(workspace) + plan.v16_offset);
-  float* parts = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + plan.parts_offset);
+  char* wsb = reinterpret_cast<char*>(workspace);
+  uint16_t* v16 = reinterpret_cast<uint16_t*>(wsb + plan.v16_offset);
+  int32_t* wplan = reinterpret_cast<int32_t*>(wsb + plan.plan_offset);
+  float* parts = reinterpret_cast<float*>(wsb + plan.parts_offset);
   {
     const int64_t n8 = (int64_t)n_layers * n_kv_heads * t_total * head_dim / 8;
     int64_t blocks = (n8 + 255) / 256;
     if (blocks > 8192) blocks = 8192;
     hipLaunchKernelGGL(v16_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n8, v_cache, v16);
   }
+  int n_wg = resident_workgroups();
+  if (n_wg > plan.n_wg_max) n_wg = plan.n_wg_max;
+  // enough tiles to keep every resident workgroup busy twice over: one tile per
+  // workgroup, no partials; otherwise balanced ranges
+  const int balanced = plan.n_tiles < 2 * n_wg;
+  if (balanced)
+    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, plan.n_tiles, plan.tile_slots,
+                       n_kv_heads, t_total, cu_seqlens, n_seqs, rows, cu_rows, rows_per_layer,
+                       plan.rows_per_tile, n_wg, plan.n_wg_max, wplan);
+  const dim3 grid(balanced ? n_wg : plan.n_tiles);
   const int log2g = ilog2(n_q_heads / n_kv_heads);
   const float c_log2 = softmax_scale * 1.4426950408889634f;
   const int out_f32 = out_dtype == KVB_F32;
-  const dim3 grid(plan.tile_slots, plan.n_split_max, n_layers * n_kv_heads);
 #define KVB_ATTN(D)                                                                              \
-  hipLaunchKernelGGL(attn_kernel<D>, grid, dim3(kThreads), 0, s, n_q_heads, n_kv_heads, log2g,   \
-                     t_total, cu_seqlens, n_seqs, rows, cu_rows, rows_per_layer,                 \
-                     plan.rows_per_tile, plan.tile_slots, plan.split_len, plan.n_split_max, q,    \
+  hipLaunchKernelGGL(attn_kernel<D>, grid, dim3(kThreads), 0, s, balanced, plan.n_tiles, n_q_heads,\
+                     n_kv_heads, log2g, t_total, cu_seqlens, n_seqs, rows, cu_rows,              \
+                     rows_per_layer, plan.rows_per_tile, plan.tile_slots, wplan, plan.n_rec, q,   \
                      k_cache, v16, c_log2, out_f32, out, parts)
 #define KVB_COMBINE(D)                                                                           \
-  hipLaunchKernelGGL(combine_kernel<D>, dim3(plan.tile_slots, n_layers * n_kv_heads, 4),         \
-                     dim3(256), 0, s, n_q_heads, n_kv_heads, log2g, t_total, cu_seqlens, n_seqs,  \
-                     rows, cu_rows, rows_per_layer, plan.rows_per_tile, plan.tile_slots,          \
-                     plan.split_len, plan.n_split_max, out_f32, out, parts)
+  hipLaunchKernelGGL(combine_kernel<D>, dim3(plan.n_tiles, kQT * (D / 8) / 256), dim3(256), 0, s, \
+                     plan.n_tiles, plan.n_wg_max, n_q_heads, n_kv_heads, log2g, t_total, rows,    \
+                     rows_per_layer, plan.tile_slots, wplan, plan.n_rec, out_f32, out, parts)
   if (head_dim == 128) {
     KVB_ATTN(128);
-    if (plan.n_split_max > 1) KVB_COMBINE(128);
+    if (balanced) KVB_COMBINE(128);
   } else {
     KVB_ATTN(64);
-    if (plan.n_split_max > 1) KVB_COMBINE(64);
+    if (balanced) KVB_COMBINE(64);
   }
 #undef KVB_ATTN
 #undef KVB_COMBINE
-  (void)max_rows;
   return hipGetLastError();
 }
 

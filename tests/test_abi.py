@@ -72,8 +72,9 @@ def test_workspace_functions_are_pure():
     assert a == 0 and kvb.kvb_select_workspace_bytes(1, 32768, 16) > 32768 * 4
     x = kvb.kvb_sparse_attn_workspace_bytes(1, 16, 2, 128, 8192, 1, 8192, 1228)
     assert x == kvb.kvb_sparse_attn_workspace_bytes(1, 16, 2, 128, 8192, 1, 8192, 1228) and x > 0
-    # no KV split for 36 layers at once: only the fp16 copy of V
-    assert kvb.kvb_sparse_attn_workspace_bytes(36, 16, 2, 128, 8192, 1, 8192, 1228) == 36 * 2 * 8192 * 128 * 2
+    # the fp16 copy of V, the work decomposition and the partial records
+    y = kvb.kvb_sparse_attn_workspace_bytes(36, 16, 2, 128, 8192, 1, 8192, 1228)
+    assert y > 36 * 2 * 8192 * 128 * 2 and y % 256 == 0
     assert kvb.kvb_sparse_attn_workspace_bytes(1, 16, 3, 128, 8192, 1, 8192, 1228) == 0
 
 

@@ -291,3 +291,50 @@ def test_attention_stage_isolated_generator_rows():
     err = np.abs(got - refo)
     _say(f"[attention-isolated] rows {len(rows)} max|err| {err.max():.3e} ws {wsb}")
     assert np.all(err <= ATOL + RTOL * np.abs(refo))
+
+
+@pytest.mark.gpu
+def test_attention_whole_tile_launch():
+    """Enough tiles (layers x kv heads x row tiles >= twice the resident
+    workgroups) that the attention takes one tile per workgroup with no
+    partial records; checked on the first and last layer."""
+    _need_gpu()
+    from paper_2608_21362_amd import kvb, pipeline
+
+    w = kw.scaled(kw.WORKLOADS["qwen_36l_8k"], n_layers=16, chunks_per_prompt=16)
+    s = kw.structure(w)
+    dev = pipeline.populate(w, s)
+    check = [0, w.n_layers - 1]
+    ref = opop.populate(w, s, layers=check)
+    rows = kw.row_subset(w, s, 528, seed=7)
+    cu_rows = np.searchsorted(rows, s.cu_seqlens).astype(np.int32)
+    T, B, L = w.t_total, len(s.cu_seqlens) - 1, w.n_layers
+    rows_per_tile = 128 // (w.n_q_heads // w.n_kv_heads)
+    n_tiles = L * w.n_kv_heads * (-(-len(rows) // rows_per_tile) + B)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    assert n_tiles >= 2 * 2 * cus, (n_tiles, cus)
+    pb = pipeline.buffers(dev)
+    pipeline.stitch(dev, pb)
+    kc, vc = pb.k_cache.clone(), pb.v_cache.clone()
+    out = torch.full((L, T, w.n_q_heads, w.head_dim), -1, dtype=torch.int16, device="cuda")
+    wsb = kvb.kvb_sparse_attn_workspace_bytes(L, w.n_q_heads, w.n_kv_heads, w.head_dim, T, B, T,
+                                              len(rows))
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    kvb.kvb_sparse_attn(L, w.n_q_heads, w.n_kv_heads, w.head_dim, T, dev.cu_seqlens, B, T,
+                        torch.from_numpy(rows).cuda(), torch.from_numpy(cu_rows).cuda(), 0,
+                        len(rows), dev.q, dev.k_fresh, dev.v_fresh, kc, vc,
+                        1.0 / np.sqrt(w.head_dim), kvb.KVB_BF16, out, ws, wsb)
+    torch.cuda.synchronize()
+    ck, cv = ref.cache_k.copy(), ref.cache_v.copy()
+    ostitch.stitch_into(ck, cv, ref.pool, ref.chunks, ref.cos, ref.sin, "bf16")
+    got_all = _np16(out)
+    for i, l in enumerate(check):
+        pk = oatt.patch(ck[i], ref.k_fresh[i], rows)
+        pv = oatt.patch(cv[i], ref.v_fresh[i], rows)
+        refo = oatt.attend_rows(ref.q[i], pk, pv, rows, s.cu_seqlens)
+        got = numerics.bf16_bits_to_f32(got_all[l][rows]).astype(np.float64)
+        err = np.abs(got - refo)
+        ratio = np.max(err / (ATOL + RTOL * np.abs(refo)))
+        _say(f"[attention-whole-tiles] layer {l} tiles {n_tiles} max|err| {err.max():.3e} "
+             f"max err/tol {ratio:.3f}")
+        assert np.all(err <= ATOL + RTOL * np.abs(refo))
