@@ -38,6 +38,7 @@
  *     (writing nothing) rather than read or write out of range.
  *   - Layouts (row-major, innermost last):
  *       cache K / V           bf16 [L][Hkv][T][d]      (T = t_total rows)
+ *       fp16 shadow of V      fp16 [L][Hkv][T][d]      (optional; see kvb_stitch)
  *       queries / outputs     bf16 [L][T][Hq][d]
  *       chunk-pool codes      u8   [P][L][Hkv][C][d*b/8]
  *       key statistics        f32  [P][L][Hkv][C/Gk][d]    (scale, zero)
@@ -45,7 +46,7 @@
  *     A row is an absolute index into the ragged batch; prompt b owns rows
  *     cu_seqlens[b] .. cu_seqlens[b+1]-1 and a row's position is its offset
  *     from cu_seqlens[b].
- *   - bfloat16 is passed as its uint16 bit pattern.
+ *   - bfloat16 and fp16 are passed as their uint16 bit patterns.
  */
 #ifndef KVB_H
 #define KVB_H
@@ -82,7 +83,8 @@ typedef struct {
   int32_t pool_idx, src_pos, dst_row, dst_pos;
 } kvb_chunk;
 
-/* 1 for this header. */
+/* 2 for this header (version 2 added the optional fp16 shadow of V to
+ * kvb_stitch, kvb_sparse_attn and kvb_sparse_attn_workspace_bytes). */
 int kvb_abi_version(void);
 
 /* Thread-local message of the last failing call on this thread. */
@@ -164,6 +166,10 @@ kvb_status kvb_kivi_quantize(const kvb_pool_layout* pool, int32_t n_pool, int32_
  * only rows of the listed chunks are written -- live rows (misses, sinks) are
  * the caller's.  Chunks must not overlap.  A chunk whose pool_idx or rows fall
  * outside the arrays is skipped.  n_pool bounds pool_idx.
+ * v_cache_f16 (optional, NULL for none; bf16 caches only): fp16 shadow of
+ * v_cache, same layout; the stitched V rows are also stored there as the fp16
+ * value of their bf16 result (exact while |v| <= 65504 and v is not below the
+ * fp16 normal range).  kvb_sparse_attn reads V from such a shadow.
  * Errors: KVB_EINVAL, KVB_EUNSUPPORTED (bits not 4/8, d not 64/128, C != 128). */
 kvb_status kvb_stitch(const kvb_pool_layout* pool, int32_t n_pool,
                       const uint8_t* k_codes, const float* k_scale, const float* k_zero,
@@ -171,7 +177,7 @@ kvb_status kvb_stitch(const kvb_pool_layout* pool, int32_t n_pool,
                       const kvb_chunk* chunks, int32_t n_chunks,
                       const float* rope_cos, const float* rope_sin,
                       int64_t t_total, kvb_dtype out_dtype, void* k_cache, void* v_cache,
-                      void* stream);
+                      uint16_t* v_cache_f16, void* stream);
 
 /* Per-token deviation (Alg. 2 step 2):
  *   delta[s][t] = 1 - (1/N) * sum cos(cache[l][h][t], fresh[l][h][t])
@@ -217,36 +223,44 @@ kvb_status kvb_deviation_topk(int32_t n_layers, int32_t n_kv_heads, int32_t head
                               int32_t* rows, int32_t* cu_rows, void* workspace,
                               size_t workspace_bytes, void* stream);
 
-/* Workspace bytes kvb_sparse_attn needs (pure function). */
+/* Workspace bytes kvb_sparse_attn needs (pure function); v_f16_given is
+ * non-zero when the call passes an fp16 shadow of V (the workspace then holds
+ * no fp16 copy of V).  0 for invalid sizes. */
 size_t kvb_sparse_attn_workspace_bytes(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads,
                                        int32_t head_dim, int64_t t_total, int32_t n_seqs,
-                                       int32_t max_seq_len, int32_t max_rows);
+                                       int32_t max_seq_len, int32_t max_rows,
+                                       int32_t v_f16_given);
 
 /* Patch then sparse-query causal attention (Alg. 2 step 4; Eq. 2).
  * For each layer l and its row set S_l (rows[l] / cu_rows[l] when
  * rows_per_layer, else rows[0] / cu_rows[0] for every layer):
  *   1. k_cache[l][h][t] = k_fresh[l][h][t] and v_cache[l][h][t] = v_fresh[l][h][t]
- *      for every t in S_l and kv head h;
+ *      for every t in S_l and kv head h (and v_cache_f16[l][h][t] = fp16 of
+ *      v_fresh[l][h][t] when the shadow is given);
  *   2. for every t in S_l and query head h, with g = floor(h * Hkv / Hq) and
  *      b the prompt of t:
  *        out[l][t][h] = sum_{u = cu_seqlens[b]}^{t} softmax_u(scale * q[l][t][h] . K[l][g][u]) V[l][g][u]
  *      over the patched cache.  q is already rotated at the row's position.
  * QK^T runs as bf16 MFMA, the softmax in float (online, base-2 exponent), PV
  * as fp16 MFMA (probabilities and values converted to fp16; |V| must stay
- * within the fp16 range), accumulation in float.  Only rows of S_l are written
+ * within the fp16 range), accumulation in float.  V is read from v_cache_f16
+ * when given (an fp16 shadow of v_cache that the caller keeps current for every
+ * row not patched here -- kvb_stitch maintains it for the stitched rows);
+ * otherwise the call converts v_cache into the workspace first.  Only rows of S_l are written
  * in out (bf16 or f32 per out_dtype, [L][t_total][Hq][d]).  max_rows bounds
  * |S_l| and max_seq_len bounds T_b (host values used to size the grid).
- * Deterministic: KV splits are combined in a fixed order.  Rows of S_l must be
- * ascending within each prompt and belong to it.
+ * Deterministic: a tile's key ranges split between workgroups are combined in
+ * key order.  Rows of S_l must be ascending within each prompt and belong to
+ * it.
  * Errors: KVB_EINVAL (incl. workspace too small, Hq % Hkv != 0),
- * KVB_EUNSUPPORTED (d not 64/128, Hq/Hkv not dividing 64). */
+ * KVB_EUNSUPPORTED (d not 64/128, Hq/Hkv not dividing 32). */
 kvb_status kvb_sparse_attn(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads,
                            int32_t head_dim, int64_t t_total, const int32_t* cu_seqlens,
                            int32_t n_seqs, int32_t max_seq_len, const int32_t* rows,
                            const int32_t* cu_rows, int32_t rows_per_layer, int32_t max_rows,
                            const uint16_t* q, const uint16_t* k_fresh, const uint16_t* v_fresh,
-                           uint16_t* k_cache, uint16_t* v_cache, float softmax_scale,
-                           kvb_dtype out_dtype, void* out, void* workspace,
+                           uint16_t* k_cache, uint16_t* v_cache, uint16_t* v_cache_f16,
+                           float softmax_scale, kvb_dtype out_dtype, void* out, void* workspace,
                            size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus

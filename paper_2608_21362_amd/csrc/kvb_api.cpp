@@ -72,7 +72,7 @@ kvb_status check_pool(const kvb_pool_layout* p) {
 
 extern "C" {
 
-int kvb_abi_version(void) { return 1; }
+int kvb_abi_version(void) { return 2; }
 
 const char* kvb_last_error(void) { return g_err.c_str(); }
 
@@ -187,7 +187,7 @@ kvb_status kvb_stitch(const kvb_pool_layout* pool, int32_t n_pool, const uint8_t
                       const float* v_scale, const float* v_zero, const kvb_chunk* chunks,
                       int32_t n_chunks, const float* rope_cos, const float* rope_sin,
                       int64_t t_total, kvb_dtype out_dtype, void* k_cache, void* v_cache,
-                      void* stream) {
+                      uint16_t* v_cache_f16, void* stream) {
   if (kvb_status s = check_pool(pool)) return s;
   REQUIRE(n_pool > 0, "n_pool must be positive");
   REQUIRE(n_chunks >= 0, "n_chunks < 0");
@@ -196,13 +196,18 @@ kvb_status kvb_stitch(const kvb_pool_layout* pool, int32_t n_pool, const uint8_t
   REQUIRE((int64_t)pool->n_layers * pool->n_kv_heads <= 65535, "n_layers * n_kv_heads > 65535");
   const void* ptrs[] = {k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, k_cache, v_cache};
   for (const void* p : ptrs) REQUIRE(p != nullptr && aligned16(p), "null or misaligned tensor");
+  if (v_cache_f16) {
+    REQUIRE(out_dtype == KVB_BF16, "an fp16 shadow of V goes with a bf16 cache");
+    REQUIRE(aligned16(v_cache_f16), "misaligned fp16 shadow of V");
+  }
   if (n_chunks == 0) return ok();
   REQUIRE(chunks != nullptr && rope_cos != nullptr && rope_sin != nullptr,
           "chunks and rotation tables are required");
   REQUIRE(aligned16(rope_cos) && aligned16(rope_sin), "rotation tables must be 16-byte aligned");
   return hip_status(kvb::launch_stitch(*pool, n_pool, k_codes, k_scale, k_zero, v_codes, v_scale,
                                        v_zero, chunks, n_chunks, rope_cos, rope_sin, t_total,
-                                       out_dtype, k_cache, v_cache, (hipStream_t)stream),
+                                       out_dtype, k_cache, v_cache, v_cache_f16,
+                                       (hipStream_t)stream),
                     "kvb_stitch");
 }
 
@@ -292,13 +297,14 @@ kvb_status kvb_deviation_topk(int32_t n_layers, int32_t n_kv_heads, int32_t head
 
 size_t kvb_sparse_attn_workspace_bytes(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads,
                                        int32_t head_dim, int64_t t_total, int32_t n_seqs,
-                                       int32_t max_seq_len, int32_t max_rows) {
+                                       int32_t max_seq_len, int32_t max_rows,
+                                       int32_t v_f16_given) {
   if (n_layers <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 || n_q_heads % n_kv_heads ||
       head_dim <= 0 || t_total <= 0 || n_seqs <= 0 || max_seq_len <= 0 || max_rows < 0)
     return 0;
   kvb::AttnPlan plan;
   if (!kvb::attn_plan(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs, max_seq_len,
-                      max_rows, &plan))
+                      max_rows, v_f16_given != 0, &plan))
     return 0;
   return plan.workspace;
 }
@@ -308,8 +314,8 @@ kvb_status kvb_sparse_attn(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_hea
                            int32_t n_seqs, int32_t max_seq_len, const int32_t* rows,
                            const int32_t* cu_rows, int32_t rows_per_layer, int32_t max_rows,
                            const uint16_t* q, const uint16_t* k_fresh, const uint16_t* v_fresh,
-                           uint16_t* k_cache, uint16_t* v_cache, float softmax_scale,
-                           kvb_dtype out_dtype, void* out, void* workspace,
+                           uint16_t* k_cache, uint16_t* v_cache, uint16_t* v_cache_f16,
+                           float softmax_scale, kvb_dtype out_dtype, void* out, void* workspace,
                            size_t workspace_bytes, void* stream) {
   if (kvb_status s = check_head_dim(head_dim)) return s;
   REQUIRE(n_layers > 0 && n_q_heads > 0 && n_kv_heads > 0, "head counts and layers must be positive");
@@ -329,10 +335,11 @@ kvb_status kvb_sparse_attn(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_hea
   for (const void* p : ptrs) REQUIRE(p != nullptr, "a required index pointer is NULL");
   const void* tens[] = {q, k_fresh, v_fresh, k_cache, v_cache, out};
   for (const void* p : tens) REQUIRE(p != nullptr && aligned16(p), "null or misaligned tensor");
+  if (v_cache_f16) REQUIRE(aligned16(v_cache_f16), "misaligned fp16 shadow of V");
   kvb::AttnPlan plan;
   if (!kvb::attn_plan(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs, max_seq_len,
-                      max_rows, &plan))
-    return fail(KVB_EUNSUPPORTED, "too many attention work items (layers x kv heads x tiles x splits)");
+                      max_rows, v_cache_f16 != nullptr, &plan))
+    return fail(KVB_EUNSUPPORTED, "too many attention work units (layers x kv heads x row tiles x key blocks)");
   REQUIRE(workspace_bytes >= plan.workspace, "workspace %zu bytes, need %zu", workspace_bytes,
           plan.workspace);
   if (plan.workspace) REQUIRE(workspace != nullptr && aligned16(workspace), "workspace NULL or misaligned");
@@ -340,8 +347,8 @@ kvb_status kvb_sparse_attn(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_hea
   return hip_status(kvb::launch_sparse_attn(plan, n_layers, n_q_heads, n_kv_heads, head_dim,
                                             t_total, cu_seqlens, n_seqs, rows, cu_rows,
                                             rows_per_layer, max_rows, q, k_fresh, v_fresh, k_cache,
-                                            v_cache, softmax_scale, out_dtype, out, workspace,
-                                            (hipStream_t)stream),
+                                            v_cache, v_cache_f16, softmax_scale, out_dtype, out,
+                                            workspace, (hipStream_t)stream),
                     "kvb_sparse_attn");
 }
 

@@ -26,7 +26,7 @@ hipError_t launch_stitch(const kvb_pool_layout& p, int32_t n_pool, const uint8_t
                          const float* v_scale, const float* v_zero, const kvb_chunk* chunks,
                          int32_t n_chunks, const float* rope_cos, const float* rope_sin,
                          int64_t t_total, kvb_dtype out_dtype, void* k_cache, void* v_cache,
-                         hipStream_t s);
+                         uint16_t* v_cache_f16, hipStream_t s);
 
 hipError_t launch_deviation(int n_layers, int n_kv_heads, int head_dim, int64_t t_total,
                             const uint16_t* k_cache, const uint16_t* k_fresh,
@@ -45,19 +45,21 @@ struct AttnPlan {
   int n_tiles;         // layers x kv heads x tile slots
   int n_wg_max;        // most attention workgroups a launch uses
   int n_rec;           // partial records (two per workgroup)
+  bool v16_in_ws;      // the fp16 copy of V lives in the workspace (no shadow given)
   size_t v16_offset;   // workspace offset of the fp16 copy of V
   size_t plan_offset;  // workspace offset of the work decomposition (int32)
   size_t parts_offset; // workspace offset of the partial records
   size_t workspace;    // total workspace bytes
 };
 bool attn_plan(int n_layers, int n_q_heads, int n_kv_heads, int head_dim, int64_t t_total,
-               int n_seqs, int max_seq_len, int max_rows, AttnPlan* plan);
+               int n_seqs, int max_seq_len, int max_rows, bool v16_given, AttnPlan* plan);
 hipError_t launch_sparse_attn(const AttnPlan& plan, int n_layers, int n_q_heads, int n_kv_heads,
                               int head_dim, int64_t t_total, const int32_t* cu_seqlens,
                               int n_seqs, const int32_t* rows, const int32_t* cu_rows,
                               int rows_per_layer, int max_rows, const uint16_t* q,
                               const uint16_t* k_fresh, const uint16_t* v_fresh,
-                              uint16_t* k_cache, uint16_t* v_cache, float softmax_scale,
-                              kvb_dtype out_dtype, void* out, void* workspace, hipStream_t s);
+                              uint16_t* k_cache, uint16_t* v_cache, uint16_t* v_cache_f16,
+                              float softmax_scale, kvb_dtype out_dtype, void* out, void* workspace,
+                              hipStream_t s);
 
 }  // namespace kvb

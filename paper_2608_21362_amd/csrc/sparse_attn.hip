@@ -1,29 +1,33 @@
 // Patch and sparse-query causal GQA attention (Alg. 2 step 4; Eq. 2).
 //
-// Per layer the call runs four kernels on one stream:
+// Per call, on one stream:
 //
 //   patch_kernel     cache[l][h][t] <- fresh[l][h][t] for every selected row t
-//                    (both tensors, every kv head; one wave per row)
-//   v16_kernel       the patched V of the layer converted to fp16 in the
-//                    workspace (exact for |v| <= 65504: a bf16 significand fits
-//                    an fp16 one), so the P.V product can take fp16 operands
-//                    straight from LDS
+//                    (both tensors, every kv head), plus the fp16 image of the
+//                    new V rows when the caller keeps an fp16 shadow of V; its
+//                    last workgroup builds the work decomposition when the
+//                    launch uses balanced ranges (below)
+//   v16_kernel       only without a shadow: V of the call converted to fp16 in
+//                    the workspace (exact for |v| <= 65504: a bf16 significand
+//                    fits an fp16 one), so the P.V product takes fp16 operands
 //   attn_kernel      the attention itself (below)
-//   combine_kernel   merges KV-split partials in split order (only when a
-//                    tile's key range was split)
+//   combine_kernel   merges the partial records of tiles that were cut between
+//                    workgroups (balanced ranges only)
 //
-// attn_kernel: one workgroup = one (layer, kv head g, tile of selected rows,
-// KV split).  The tile packs rows x the G = Hq/Hkv query heads that share kv
-// head g into the MFMA N dimension: each of the 4 waves owns 32 query vectors
-// (32/G rows x G heads).  Keys stream in blocks of 64 through a two-stage LDS
-// ring filled by asynchronous global->LDS loads (no VGPR staging), XOR-swizzled
-// on 16-byte chunks so the operand reads below are free of bank conflicts:
+// attn_kernel: a tile is up to 128 / G selected rows of one prompt for one
+// (layer, kv head g): rows x the G = Hq/Hkv query heads that share kv head g
+// fill the MFMA N dimension, each of the 4 waves owning 32 query vectors
+// (32/G rows x G heads).  A workgroup runs one whole tile, or a range of key
+// blocks that may span tiles (see attn_kernel).  Keys stream in blocks of 32
+// through a four-stage LDS ring filled by asynchronous global->LDS loads (no
+// VGPR staging), XOR-swizzled on 16-byte chunks so the operand reads below are
+// free of bank conflicts:
 //
-//   S^T (64 keys x 32 queries) = K Q^T     bf16 MFMA 32x32x16: K rows from LDS
+//   S^T (32 keys x 32 queries) = K Q^T     bf16 MFMA 32x32x16: K rows from LDS
 //                                           (A operand), Q^T kept in VGPRs
 //   online softmax over keys               fp32, base-2 exponent.  Each lane
-//                                           holds 32 scores of one query, the
-//                                           other 32 sit in lane ^ 32.  The
+//                                           holds 16 scores of one query, the
+//                                           other 16 sit in lane ^ 32.  The
 //                                           running maximum is refreshed only
 //                                           when a block raises it by more
 //                                           than 8 (log2 units), so partial
@@ -32,6 +36,9 @@
 //                                           the row-major fp16 V block with the
 //                                           LDS transpose read, P^T converted
 //                                           from the S^T accumulators
+//
+// The loop is software-pipelined: the scores of block j+1 are computed while
+// block j's probabilities are formed, with one barrier per block.
 //
 // The accumulator layout of a 32x32 MFMA gives lane half h the keys
 // {4h..4h+3, 8+4h..8+4h+3} of every 16-key step; the transpose reads fetch V
@@ -89,51 +96,15 @@ __device__ __forceinline__ void wait_lgkmcnt0() {
 // s_barrier builtin is not a memory barrier for it); emits no instruction.
 __device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
 
-// ---------------------------------------------------------------- patch ----
-__global__ void __launch_bounds__(256)
-patch_kernel(int32_t L, int32_t Hkv, int32_t D, int64_t t_total, int32_t n_seqs,
-             const int32_t* __restrict__ rows, const int32_t* __restrict__ cu_rows,
-             int32_t rows_per_layer, int32_t max_rows, const uint16_t* __restrict__ kf,
-             const uint16_t* __restrict__ vf, uint16_t* __restrict__ kc,
-             uint16_t* __restrict__ vc) {
-  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
-  const int lane = threadIdx.x & 63;
-  const int64_t l = wave / max_rows;
-  const int64_t i = wave % max_rows;
-  if (l >= L) return;
-  const int64_t set = rows_per_layer ? l : 0;
-  const int32_t n = cu_rows[set * (n_seqs + 1) + n_seqs];
-  if (i >= n) return;
-  const int64_t t = rows[set * t_total + i];
-  if (t < 0 || t >= t_total) return;
-  const int chunks = D / 8;  // 16-byte pieces per head row
-  for (int e = lane; e < 2 * Hkv * chunks; e += 64) {
-    const int tensor = e / (Hkv * chunks);
-    const int h = (e / chunks) % Hkv;
-    const int c = e % chunks;
-    const int64_t off = (((l * Hkv + h) * t_total) + t) * D + c * 8;
-    if (tensor == 0)
-      *reinterpret_cast<uint4*>(kc + off) = *reinterpret_cast<const uint4*>(kf + off);
-    else
-      *reinterpret_cast<uint4*>(vc + off) = *reinterpret_cast<const uint4*>(vf + off);
-  }
-}
-
 // ------------------------------------------------------------ V to fp16 ----
-__device__ __forceinline__ uint32_t bf16pair_to_f16pair(uint32_t w) {
-  f32x2 f = {bf16_lo(w), bf16_hi(w)};
-  f16x2 h = __builtin_convertvector(f, f16x2);
-  return __builtin_bit_cast(uint32_t, h);
-}
-
 __global__ void __launch_bounds__(256)
 v16_kernel(int64_t n8, const uint16_t* __restrict__ v, uint16_t* __restrict__ v16) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n8;
        i += (int64_t)gridDim.x * blockDim.x) {
     const uint4 a = reinterpret_cast<const uint4*>(v)[i];
     reinterpret_cast<uint4*>(v16)[i] =
-        make_uint4(bf16pair_to_f16pair(a.x), bf16pair_to_f16pair(a.y),
-                   bf16pair_to_f16pair(a.z), bf16pair_to_f16pair(a.w));
+        make_uint4(bf16x2_to_f16x2(a.x), bf16x2_to_f16x2(a.y),
+                   bf16x2_to_f16x2(a.z), bf16x2_to_f16x2(a.w));
   }
 }
 
@@ -560,21 +531,21 @@ __host__ __device__ constexpr int64_t tile_meta_offset(int64_t n_tiles, int64_t 
 //   plan[3+n_tiles .. 3+n_tiles+n_wg) = tile holding unit w C,
 //   then per tile an int4 {first row entry, end row entry, key start, key end}
 //   at the 16-byte aligned offset tile_meta_offset(n_tiles, n_wg_max).
-__global__ void __launch_bounds__(1024)
-plan_kernel(int32_t n_tiles, int32_t tile_slots, int32_t Hkv, int64_t t_total,
-            const int32_t* __restrict__ cu_seqlens, int32_t n_seqs,
-            const int32_t* __restrict__ rows, const int32_t* __restrict__ cu_rows,
-            int32_t rows_per_layer, int32_t rows_per_tile, int32_t n_wg, int32_t n_wg_max,
-            int32_t* __restrict__ plan) {
-  int4* meta = reinterpret_cast<int4*>(plan + tile_meta_offset(n_tiles, n_wg_max));
+__device__ __forceinline__ void build_plan(
+    int32_t n_tiles, int32_t tile_slots, int32_t Hkv, int64_t t_total,
+    const int32_t* __restrict__ cu_seqlens, int32_t n_seqs, const int32_t* __restrict__ rows,
+    const int32_t* __restrict__ cu_rows, int32_t rows_per_layer, int32_t rows_per_tile,
+    int32_t n_wg, int32_t n_wg_max, int32_t* __restrict__ plan) {
   __shared__ int warp_sums[16];
   __shared__ int carry_sh;
   int32_t* prefix = plan + 2;
   int32_t* first = plan + 3 + n_tiles;
+  int4* meta = reinterpret_cast<int4*>(plan + tile_meta_offset(n_tiles, n_wg_max));
+  const int nt = blockDim.x;  // a multiple of 64, at most 1024
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   if (tid == 0) carry_sh = 0;
   __syncthreads();
-  for (int base = 0; base < n_tiles; base += 1024) {
+  for (int base = 0; base < n_tiles; base += nt) {
     const int t = base + tid;
     int nb = 0;
     if (t < n_tiles) {
@@ -591,7 +562,7 @@ plan_kernel(int32_t n_tiles, int32_t tile_slots, int32_t Hkv, int64_t t_total,
       }
       meta[t] = mt;
     }
-    // inclusive scan over the 1024 threads: within each wave, then over waves
+    // inclusive scan over the block: within each wave, then over waves
     int x = nb;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
@@ -604,7 +575,7 @@ plan_kernel(int32_t n_tiles, int32_t tile_slots, int32_t Hkv, int64_t t_total,
     for (int i = 0; i < wv; ++i) before += warp_sums[i];
     if (t < n_tiles) prefix[t] = before + x - nb;
     __syncthreads();
-    if (tid == 1023) carry_sh = before + x;
+    if (tid == nt - 1) carry_sh = before + x;
     __syncthreads();
   }
   const int total = carry_sh;
@@ -615,16 +586,60 @@ plan_kernel(int32_t n_tiles, int32_t tile_slots, int32_t Hkv, int64_t t_total,
     prefix[n_tiles] = total;
   }
   __syncthreads();
-  // tile holding unit w * chunk: the last t with prefix[t] <= w * chunk and a
-  // non-empty range
-  for (int w = tid; w < n_wg; w += 1024) {
+  // tile holding unit w * chunk: the largest t with prefix[t] <= w * chunk
+  for (int w = tid; w < n_wg; w += nt) {
     const int u = w * chunk;
-    int lo = 0, hi = n_tiles - 1;  // find the largest t with prefix[t] <= u
+    int lo = 0, hi = n_tiles - 1;
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
       if (prefix[mid] <= u) lo = mid; else hi = mid - 1;
     }
     first[w] = lo;
+  }
+}
+
+// Patch: cache[l][h][t] <- fresh[l][h][t] for every selected row t (both
+// tensors, every kv head; one wave per row), with the fp16 image of the new V
+// rows when the caller keeps an fp16 shadow of V.  With plan != NULL the last
+// workgroup builds the work decomposition instead.
+__global__ void __launch_bounds__(256)
+patch_kernel(int32_t L, int32_t Hkv, int32_t D, int64_t t_total, int32_t n_seqs,
+             const int32_t* __restrict__ rows, const int32_t* __restrict__ cu_rows,
+             int32_t rows_per_layer, int32_t max_rows, const uint16_t* __restrict__ kf,
+             const uint16_t* __restrict__ vf, uint16_t* __restrict__ kc,
+             uint16_t* __restrict__ vc, uint16_t* __restrict__ vh,
+             const int32_t* __restrict__ cu_seqlens, int32_t n_tiles, int32_t tile_slots,
+             int32_t rows_per_tile, int32_t n_wg, int32_t n_wg_max, int32_t* __restrict__ plan) {
+  if (plan != nullptr && blockIdx.x == gridDim.x - 1) {
+    build_plan(n_tiles, tile_slots, Hkv, t_total, cu_seqlens, n_seqs, rows, cu_rows,
+               rows_per_layer, rows_per_tile, n_wg, n_wg_max, plan);
+    return;
+  }
+  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int lane = threadIdx.x & 63;
+  const int64_t l = wave / max_rows;
+  const int64_t i = wave % max_rows;
+  if (l >= L) return;
+  const int64_t set = rows_per_layer ? l : 0;
+  const int32_t n = cu_rows[set * (n_seqs + 1) + n_seqs];
+  if (i >= n) return;
+  const int64_t t = rows[set * t_total + i];
+  if (t < 0 || t >= t_total) return;
+  const int chunks = D / 8;  // 16-byte pieces per head row
+  for (int e = lane; e < 2 * Hkv * chunks; e += 64) {
+    const int tensor = e / (Hkv * chunks);
+    const int h = (e / chunks) % Hkv;
+    const int c = e % chunks;
+    const int64_t off = (((l * Hkv + h) * t_total) + t) * D + c * 8;
+    if (tensor == 0) {
+      *reinterpret_cast<uint4*>(kc + off) = *reinterpret_cast<const uint4*>(kf + off);
+    } else {
+      const uint4 a = *reinterpret_cast<const uint4*>(vf + off);
+      *reinterpret_cast<uint4*>(vc + off) = a;
+      if (vh)
+        *reinterpret_cast<uint4*>(vh + off) = make_uint4(bf16x2_to_f16x2(a.x), bf16x2_to_f16x2(a.y),
+                                                         bf16x2_to_f16x2(a.z), bf16x2_to_f16x2(a.w));
+    }
   }
 }
 
@@ -785,7 +800,7 @@ int ilog2(int x) {
 }  // namespace
 
 bool attn_plan(int n_layers, int n_q_heads, int n_kv_heads, int head_dim, int64_t t_total,
-               int n_seqs, int max_seq_len, int max_rows, AttnPlan* plan) {
+               int n_seqs, int max_seq_len, int max_rows, bool v16_given, AttnPlan* plan) {
   const int G = n_q_heads / n_kv_heads;
   const int rows_per_tile = kQT / G;
   const int64_t full_tiles = ((int64_t)max_rows + rows_per_tile - 1) / rows_per_tile;
@@ -798,7 +813,9 @@ bool attn_plan(int n_layers, int n_q_heads, int n_kv_heads, int head_dim, int64_
   plan->n_tiles = (int)n_tiles;
   plan->n_wg_max = kAttnMaxWorkgroups;
   plan->n_rec = 2 * kAttnMaxWorkgroups;
-  const size_t v16 = (size_t)n_layers * n_kv_heads * (size_t)t_total * head_dim * 2;
+  plan->v16_in_ws = !v16_given;
+  const size_t v16 =
+      v16_given ? 0 : (size_t)n_layers * n_kv_heads * (size_t)t_total * head_dim * 2;
   const size_t plan_ints = (size_t)tile_meta_offset(n_tiles, plan->n_wg_max) + 4 * (size_t)n_tiles;
   const size_t parts = (size_t)(head_dim == 128 ? rec_ml_offset<128>(plan->n_rec)
                                                  : rec_ml_offset<64>(plan->n_rec)) +
@@ -817,39 +834,39 @@ hipError_t launch_sparse_attn(const AttnPlan& plan, int n_layers, int n_q_heads,
                               int n_seqs, const int32_t* rows, const int32_t* cu_rows,
                               int rows_per_layer, int max_rows, const uint16_t* q,
                               const uint16_t* k_fresh, const uint16_t* v_fresh,
-                              uint16_t* k_cache, uint16_t* v_cache, float softmax_scale,
-                              kvb_dtype out_dtype, void* out, void* workspace, hipStream_t s) {
-  {
-    const int64_t waves = (int64_t)n_layers * max_rows;
-    const int64_t blocks = (waves * 64 + 255) / 256;
-    if (blocks > 0)
-      hipLaunchKernelGGL(patch_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n_layers,
-                         n_kv_heads, head_dim, t_total, n_seqs, rows, cu_rows, rows_per_layer,
-                         max_rows, k_fresh, v_fresh, k_cache, v_cache);
-  }
+                              uint16_t* k_cache, uint16_t* v_cache, uint16_t* v_cache_f16,
+                              float softmax_scale, kvb_dtype out_dtype, void* out, void* workspace,
+                              hipStream_t s) {
   char* wsb = reinterpret_cast<char*>(workspace);
-  uint16_t* v16 = reinterpret_cast<uint16_t*>(wsb + plan.v16_offset);
+  uint16_t* v16 = plan.v16_in_ws ? reinterpret_cast<uint16_t*>(wsb + plan.v16_offset) : v_cache_f16;
   int32_t* wplan = reinterpret_cast<int32_t*>(wsb + plan.plan_offset);
   float* parts = reinterpret_cast<float*>(wsb + plan.parts_offset);
-  {
-    const int64_t n8 = (int64_t)n_layers * n_kv_heads * t_total * head_dim / 8;
-    int64_t blocks = (n8 + 255) / 256;
-    if (blocks > 8192) blocks = 8192;
-    hipLaunchKernelGGL(v16_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n8, v_cache, v16);
-  }
   int n_wg = resident_workgroups();
   if (n_wg > plan.n_wg_max) n_wg = plan.n_wg_max;
   // enough tiles to keep every resident workgroup busy twice over: one tile per
   // workgroup, no partials; otherwise balanced ranges
   const int balanced = plan.n_tiles < 2 * n_wg;
-  if (balanced)
-    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, plan.n_tiles, plan.tile_slots,
-                       n_kv_heads, t_total, cu_seqlens, n_seqs, rows, cu_rows, rows_per_layer,
-                       plan.rows_per_tile, n_wg, plan.n_wg_max, wplan);
-  const dim3 grid(balanced ? n_wg : plan.n_tiles);
+  {
+    const int64_t waves = (int64_t)n_layers * max_rows;
+    const int64_t blocks = (waves * 64 + 255) / 256 + (balanced ? 1 : 0);
+    if (blocks > 0)
+      hipLaunchKernelGGL(patch_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n_layers,
+                         n_kv_heads, head_dim, t_total, n_seqs, rows, cu_rows, rows_per_layer,
+                         max_rows, k_fresh, v_fresh, k_cache, v_cache,
+                         plan.v16_in_ws ? nullptr : v_cache_f16, cu_seqlens, plan.n_tiles,
+                         plan.tile_slots, plan.rows_per_tile, n_wg, plan.n_wg_max,
+                         balanced ? wplan : nullptr);
+  }
+  if (plan.v16_in_ws) {
+    const int64_t n8 = (int64_t)n_layers * n_kv_heads * t_total * head_dim / 8;
+    int64_t blocks = (n8 + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    hipLaunchKernelGGL(v16_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n8, v_cache, v16);
+  }
   const int log2g = ilog2(n_q_heads / n_kv_heads);
   const float c_log2 = softmax_scale * 1.4426950408889634f;
   const int out_f32 = out_dtype == KVB_F32;
+  const dim3 grid(balanced ? n_wg : plan.n_tiles);
 #define KVB_ATTN(D)                                                                              \
   hipLaunchKernelGGL(attn_kernel<D>, grid, dim3(kThreads), 0, s, balanced, plan.n_tiles, n_q_heads,\
                      n_kv_heads, log2g, t_total, cu_seqlens, n_seqs, rows, cu_rows,              \

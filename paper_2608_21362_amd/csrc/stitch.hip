@@ -11,6 +11,9 @@
 // one thread takes one token and 16 consecutive channels (one statistic group,
 // Gv % 16 == 0).
 //
+// With a non-NULL fp16 shadow the value jobs also store the fp16 image of the
+// bfloat16 values (the operand the attention's P.V product reads).
+//
 // Arithmetic is double with contraction off: x = fma(code, scale, zero) is
 // exact in the product (8-bit code times 24-bit scale), so it equals the
 // product-then-sum form; the rotation is mul, mul, sub / add.  The double is
@@ -31,7 +34,7 @@ stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
               const float* __restrict__ v_scale, const float* __restrict__ v_zero,
               const kvb_chunk* __restrict__ chunks, const float* __restrict__ rope_cos,
               const float* __restrict__ rope_sin, int64_t t_total, void* __restrict__ k_out,
-              void* __restrict__ v_out) {
+              void* __restrict__ v_out, uint16_t* __restrict__ v16_out) {
   constexpr int H = D / 2;
   constexpr int CB = D * BITS / 8;       // code bytes per token row
   constexpr int TPT = H / 8;             // key threads per token quad
@@ -146,6 +149,14 @@ stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
         B.z = pack_bf16x2(y[12], y[13]); B.w = pack_bf16x2(y[14], y[15]);
         *reinterpret_cast<uint4*>(vo) = A;
         *reinterpret_cast<uint4*>(vo + 8) = B;
+        if (v16_out) {
+          // fp16 image of the bf16 values just written
+          uint16_t* ho = v16_out + o;
+          *reinterpret_cast<uint4*>(ho) = make_uint4(bf16x2_to_f16x2(A.x), bf16x2_to_f16x2(A.y),
+                                                     bf16x2_to_f16x2(A.z), bf16x2_to_f16x2(A.w));
+          *reinterpret_cast<uint4*>(ho + 8) = make_uint4(bf16x2_to_f16x2(B.x), bf16x2_to_f16x2(B.y),
+                                                         bf16x2_to_f16x2(B.z), bf16x2_to_f16x2(B.w));
+        }
       } else {
         float* vo = reinterpret_cast<float*>(v_out) + o;
 #pragma unroll
@@ -163,13 +174,13 @@ hipError_t launch_stitch(const kvb_pool_layout& p, int32_t n_pool, const uint8_t
                          const float* v_scale, const float* v_zero, const kvb_chunk* chunks,
                          int32_t n_chunks, const float* rope_cos, const float* rope_sin,
                          int64_t t_total, kvb_dtype out_dtype, void* k_cache, void* v_cache,
-                         hipStream_t s) {
+                         uint16_t* v_cache_f16, hipStream_t s) {
   const dim3 grid(n_chunks, p.n_layers * p.n_kv_heads), block(256);
   const bool bf = out_dtype == KVB_BF16;
 #define KVB_STITCH(B, D, F)                                                                       \
   hipLaunchKernelGGL((stitch_kernel<B, D, F>), grid, block, 0, s, p.n_layers, p.n_kv_heads,      \
                      p.k_group, p.v_group, n_pool, k_codes, k_scale, k_zero, v_codes, v_scale,   \
-                     v_zero, chunks, rope_cos, rope_sin, t_total, k_cache, v_cache)
+                     v_zero, chunks, rope_cos, rope_sin, t_total, k_cache, v_cache, v_cache_f16)
   if (p.bits == 8) {
     if (p.head_dim == 128) { if (bf) KVB_STITCH(8, 128, true); else KVB_STITCH(8, 128, false); }
     else { if (bf) KVB_STITCH(8, 64, true); else KVB_STITCH(8, 64, false); }

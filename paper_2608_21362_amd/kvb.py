@@ -48,15 +48,17 @@ _SIGS = {
     "kvb_kivi_quantize": (_i32, [ctypes.POINTER(kvb_pool_layout), _i32, _i32, _i32, _i32, _vp, _vp,
                                  _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "kvb_stitch": (_i32, [ctypes.POINTER(kvb_pool_layout), _i32, _vp, _vp, _vp, _vp, _vp, _vp,
-                          _vp, _i32, _vp, _vp, _i64, _i32, _vp, _vp, _vp]),
+                          _vp, _i32, _vp, _vp, _i64, _i32, _vp, _vp, _vp, _vp]),
     "kvb_deviation": (_i32, [_i32, _i32, _i32, _i64, _vp, _vp, _vp, _vp, _i32, _vp, _vp]),
     "kvb_select_workspace_bytes": (_sz, [_i32, _i64, _i32]),
     "kvb_select": (_i32, [_i32, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "kvb_deviation_topk": (_i32, [_i32, _i32, _i32, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _i32,
                                   _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
-    "kvb_sparse_attn_workspace_bytes": (_sz, [_i32, _i32, _i32, _i32, _i64, _i32, _i32, _i32]),
+    "kvb_sparse_attn_workspace_bytes": (_sz, [_i32, _i32, _i32, _i32, _i64, _i32, _i32, _i32,
+                                              _i32]),
     "kvb_sparse_attn": (_i32, [_i32, _i32, _i32, _i32, _i64, _vp, _i32, _i32, _vp, _vp, _i32,
-                               _i32, _vp, _vp, _vp, _vp, _vp, _f32, _i32, _vp, _vp, _sz, _vp]),
+                               _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _i32, _vp, _vp, _sz,
+                               _vp]),
 }
 
 
@@ -154,11 +156,12 @@ def kvb_kivi_quantize(pool, n_pool, first_layer, n_in, in_dtype, k_in, v_in, k_c
 # ---- the hot path -------------------------------------------------------------
 
 def kvb_stitch(pool, n_pool, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, chunks,
-               n_chunks, rope_cos, rope_sin, t_total, out_dtype, k_cache, v_cache, stream=None):
+               n_chunks, rope_cos, rope_sin, t_total, out_dtype, k_cache, v_cache, v_cache_f16,
+               stream=None):
     _check(_lib.kvb_stitch(ctypes.byref(pool), n_pool, _p(k_codes), _p(k_scale), _p(k_zero),
                            _p(v_codes), _p(v_scale), _p(v_zero), _p(chunks), n_chunks,
                            _p(rope_cos), _p(rope_sin), t_total, out_dtype, _p(k_cache),
-                           _p(v_cache), _stream(stream)))
+                           _p(v_cache), _p(v_cache_f16), _stream(stream)))
 
 
 def kvb_deviation(n_layers, n_kv_heads, head_dim, t_total, k_cache, k_fresh, v_cache, v_fresh,
@@ -190,17 +193,18 @@ def kvb_deviation_topk(n_layers, n_kv_heads, head_dim, t_total, cu_seqlens, n_se
 
 
 def kvb_sparse_attn_workspace_bytes(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs,
-                                    max_seq_len, max_rows) -> int:
+                                    max_seq_len, max_rows, v_f16_given) -> int:
     return _lib.kvb_sparse_attn_workspace_bytes(n_layers, n_q_heads, n_kv_heads, head_dim, t_total,
-                                                n_seqs, max_seq_len, max_rows)
+                                                n_seqs, max_seq_len, max_rows, int(v_f16_given))
 
 
 def kvb_sparse_attn(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, cu_seqlens, n_seqs,
                     max_seq_len, rows, cu_rows, rows_per_layer, max_rows, q, k_fresh, v_fresh,
-                    k_cache, v_cache, softmax_scale, out_dtype, out, workspace, workspace_bytes,
-                    stream=None):
+                    k_cache, v_cache, v_cache_f16, softmax_scale, out_dtype, out, workspace,
+                    workspace_bytes, stream=None):
     _check(_lib.kvb_sparse_attn(n_layers, n_q_heads, n_kv_heads, head_dim, t_total,
                                 _p(cu_seqlens), n_seqs, max_seq_len, _p(rows), _p(cu_rows),
                                 int(rows_per_layer), max_rows, _p(q), _p(k_fresh), _p(v_fresh),
-                                _p(k_cache), _p(v_cache), float(softmax_scale), out_dtype, _p(out),
-                                _p(workspace), workspace_bytes, _stream(stream)))
+                                _p(k_cache), _p(v_cache), _p(v_cache_f16), float(softmax_scale),
+                                out_dtype, _p(out), _p(workspace), workspace_bytes,
+                                _stream(stream)))

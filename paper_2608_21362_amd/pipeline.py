@@ -145,6 +145,7 @@ def populate(w: kw.Workload, s: kw.Structure, layers=None, with_q=True, draws_fn
 class PathBuffers:
     k_cache: torch.Tensor
     v_cache: torch.Tensor
+    v_cache_f16: torch.Tensor  # fp16 shadow of v_cache, kept by kvb_stitch and kvb_sparse_attn
     delta: torch.Tensor
     rows: torch.Tensor
     cu_rows: torch.Tensor
@@ -161,9 +162,9 @@ def buffers(di: DeviceInputs, out_dtype=kvb.KVB_BF16, attn_all_layers=False) -> 
     B = len(di.s.cu_seqlens) - 1
     sel_bytes = kvb.kvb_select_workspace_bytes(di.n_sets, T, B)
     per_layer_ws = kvb.kvb_sparse_attn_workspace_bytes(1, w.n_q_heads, w.n_kv_heads, w.head_dim, T,
-                                                       B, di.max_seq_len, di.max_rows)
+                                                       B, di.max_seq_len, di.max_rows, 1)
     all_ws = kvb.kvb_sparse_attn_workspace_bytes(L, w.n_q_heads, w.n_kv_heads, w.head_dim, T, B,
-                                                 di.max_seq_len, di.max_rows)
+                                                 di.max_seq_len, di.max_rows, 1)
     attn_bytes = max(per_layer_ws, all_ws if attn_all_layers else 0)
     odt = torch.int16 if out_dtype == kvb.KVB_BF16 else torch.float32
     out = torch.full((L, T, w.n_q_heads, w.head_dim), -1, dtype=odt, device="cuda")
@@ -173,6 +174,9 @@ def buffers(di: DeviceInputs, out_dtype=kvb.KVB_BF16, attn_all_layers=False) -> 
         out.fill_(float("nan"))
     return PathBuffers(
         k_cache=di.cache_init_k.clone(), v_cache=di.cache_init_v.clone(),
+        # every prompt row is stitched (cached chunk) or selected (live rows are
+        # always selected), so each step rewrites the whole shadow
+        v_cache_f16=torch.zeros_like(di.cache_init_v),
         delta=torch.zeros((di.n_sets, T), dtype=torch.float32, device="cuda"),
         rows=torch.full((di.n_sets, T), -1, dtype=torch.int32, device="cuda"),
         cu_rows=torch.zeros((di.n_sets, B + 1), dtype=torch.int32, device="cuda"),
@@ -184,10 +188,12 @@ def buffers(di: DeviceInputs, out_dtype=kvb.KVB_BF16, attn_all_layers=False) -> 
 
 def stitch(di: DeviceInputs, pb: PathBuffers, out_dtype=kvb.KVB_BF16, k_out=None, v_out=None,
            stream=None):
+    own = k_out is None and v_out is None and out_dtype == kvb.KVB_BF16
     kvb.kvb_stitch(di.pool, di.n_pool, di.k_codes, di.k_scale, di.k_zero, di.v_codes, di.v_scale,
                    di.v_zero, di.chunks, di.n_pool, di.rope_cos, di.rope_sin, di.w.t_total,
                    out_dtype, pb.k_cache if k_out is None else k_out,
-                   pb.v_cache if v_out is None else v_out, stream)
+                   pb.v_cache if v_out is None else v_out, pb.v_cache_f16 if own else None,
+                   stream)
 
 
 def deviation_topk(di: DeviceInputs, pb: PathBuffers, stream=None):
@@ -207,7 +213,8 @@ def sparse_attn_layer(di: DeviceInputs, pb: PathBuffers, i: int, out_dtype=kvb.K
     kvb.kvb_sparse_attn(1, w.n_q_heads, w.n_kv_heads, w.head_dim, T, di.cu_seqlens, B,
                         di.max_seq_len, pb.rows[si], pb.cu_rows[si], 0, di.max_rows, di.q[i],
                         di.k_fresh[i], di.v_fresh[i], pb.k_cache[i], pb.v_cache[i],
-                        1.0 / float(np.sqrt(w.head_dim)), out_dtype, pb.out[i], pb.attn_ws,
+                        pb.v_cache_f16[i], 1.0 / float(np.sqrt(w.head_dim)), out_dtype, pb.out[i],
+                        pb.attn_ws,
                         pb.attn_ws_bytes, stream)
 
 
@@ -217,7 +224,7 @@ def sparse_attn_all(di: DeviceInputs, pb: PathBuffers, out_dtype=kvb.KVB_BF16, s
     B = len(di.s.cu_seqlens) - 1
     kvb.kvb_sparse_attn(di.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, T, di.cu_seqlens, B,
                         di.max_seq_len, pb.rows, pb.cu_rows, int(w.per_layer), di.max_rows, di.q,
-                        di.k_fresh, di.v_fresh, pb.k_cache, pb.v_cache,
+                        di.k_fresh, di.v_fresh, pb.k_cache, pb.v_cache, pb.v_cache_f16,
                         1.0 / float(np.sqrt(w.head_dim)), out_dtype, pb.out, pb.attn_ws,
                         pb.attn_ws_bytes_all, stream)
 

@@ -33,7 +33,7 @@ def test_every_declared_symbol_is_exported():
     for n in names:
         assert hasattr(lib, n), n
     assert sorted(names) == sorted(kvb.EXPORTED)
-    assert kvb.kvb_abi_version() == 1
+    assert kvb.kvb_abi_version() == 2
 
 
 @pytest.mark.parametrize("theta,d", [(1e4, 64), (1e6, 128)])
@@ -70,12 +70,15 @@ def test_host_helper_errors():
 def test_workspace_functions_are_pure():
     a = kvb.kvb_select_workspace_bytes(36, 8192, 1)
     assert a == 0 and kvb.kvb_select_workspace_bytes(1, 32768, 16) > 32768 * 4
-    x = kvb.kvb_sparse_attn_workspace_bytes(1, 16, 2, 128, 8192, 1, 8192, 1228)
-    assert x == kvb.kvb_sparse_attn_workspace_bytes(1, 16, 2, 128, 8192, 1, 8192, 1228) and x > 0
-    # the fp16 copy of V, the work decomposition and the partial records
-    y = kvb.kvb_sparse_attn_workspace_bytes(36, 16, 2, 128, 8192, 1, 8192, 1228)
+    x = kvb.kvb_sparse_attn_workspace_bytes(1, 16, 2, 128, 8192, 1, 8192, 1228, 0)
+    assert x == kvb.kvb_sparse_attn_workspace_bytes(1, 16, 2, 128, 8192, 1, 8192, 1228, 0) and x > 0
+    # the fp16 copy of V (unless the caller keeps a shadow), the work
+    # decomposition and the partial records
+    y = kvb.kvb_sparse_attn_workspace_bytes(36, 16, 2, 128, 8192, 1, 8192, 1228, 0)
+    y16 = kvb.kvb_sparse_attn_workspace_bytes(36, 16, 2, 128, 8192, 1, 8192, 1228, 1)
     assert y > 36 * 2 * 8192 * 128 * 2 and y % 256 == 0
-    assert kvb.kvb_sparse_attn_workspace_bytes(1, 16, 3, 128, 8192, 1, 8192, 1228) == 0
+    assert y - y16 >= 36 * 2 * 8192 * 128 * 2 and y16 > 0
+    assert kvb.kvb_sparse_attn_workspace_bytes(1, 16, 3, 128, 8192, 1, 8192, 1228, 0) == 0
 
 
 def _pool(**kw_):
@@ -87,7 +90,8 @@ def _pool(**kw_):
 def _stitch(**over):
     args = dict(pool=_pool(), n_pool=1, k_codes=FAKE, k_scale=FAKE, k_zero=FAKE, v_codes=FAKE,
                 v_scale=FAKE, v_zero=FAKE, chunks=FAKE, n_chunks=1, rope_cos=FAKE, rope_sin=FAKE,
-                t_total=128, out_dtype=kvb.KVB_BF16, k_cache=FAKE, v_cache=FAKE, stream=0)
+                t_total=128, out_dtype=kvb.KVB_BF16, k_cache=FAKE, v_cache=FAKE, v_cache_f16=None,
+                stream=0)
     args.update(over)
     kvb.kvb_stitch(**args)
 
@@ -104,6 +108,8 @@ def _stitch(**over):
     (dict(t_total=2**31), kvb.KVB_EINVAL),
     (dict(out_dtype=kvb.KVB_F64), kvb.KVB_EINVAL),
     (dict(rope_cos=None), kvb.KVB_EINVAL),
+    (dict(v_cache_f16=FAKE + 2), kvb.KVB_EINVAL),
+    (dict(v_cache_f16=FAKE, out_dtype=kvb.KVB_F32), kvb.KVB_EINVAL),  # shadow needs a bf16 cache
 ])
 def test_stitch_rejects(over, status):
     with pytest.raises(kvb.KvbError) as e:
@@ -146,13 +152,15 @@ def _attn(**over):
     args = dict(n_layers=1, n_q_heads=16, n_kv_heads=2, head_dim=128, t_total=4096,
                 cu_seqlens=FAKE, n_seqs=1, max_seq_len=4096, rows=FAKE, cu_rows=FAKE,
                 rows_per_layer=0, max_rows=600, q=FAKE, k_fresh=FAKE, v_fresh=FAKE,
-                k_cache=FAKE, v_cache=FAKE, softmax_scale=0.088, out_dtype=kvb.KVB_BF16, out=FAKE,
+                k_cache=FAKE, v_cache=FAKE, v_cache_f16=None, softmax_scale=0.088,
+                out_dtype=kvb.KVB_BF16, out=FAKE,
                 workspace=FAKE, workspace_bytes=0, stream=0)
     args.update(over)
     if "workspace_bytes" not in over:
         args["workspace_bytes"] = kvb.kvb_sparse_attn_workspace_bytes(
             args["n_layers"], args["n_q_heads"], args["n_kv_heads"], max(args["head_dim"], 1),
-            args["t_total"], max(args["n_seqs"], 1), max(args["max_seq_len"], 1), args["max_rows"])
+            args["t_total"], max(args["n_seqs"], 1), max(args["max_seq_len"], 1), args["max_rows"],
+            args["v_cache_f16"] is not None)
     kvb.kvb_sparse_attn(**args)
 
 
@@ -168,6 +176,7 @@ def _attn(**over):
     (dict(max_rows=5000), kvb.KVB_EINVAL),
     (dict(softmax_scale=0.0), kvb.KVB_EINVAL),
     (dict(out_dtype=7), kvb.KVB_EINVAL),
+    (dict(v_cache_f16=FAKE + 2), kvb.KVB_EINVAL),
 ])
 def test_sparse_attn_rejects(over, status):
     with pytest.raises(kvb.KvbError) as e:

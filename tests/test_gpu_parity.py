@@ -275,10 +275,10 @@ def test_attention_stage_isolated_generator_rows():
     out = torch.full((1, T, w.n_q_heads, w.head_dim), -1, dtype=torch.int16, device="cuda")
     max_seq = int(np.max(np.diff(s.cu_seqlens)))
     wsb = kvb.kvb_sparse_attn_workspace_bytes(1, w.n_q_heads, w.n_kv_heads, w.head_dim, T, B,
-                                              max_seq, len(rows))
+                                              max_seq, len(rows), 0)
     ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
     kvb.kvb_sparse_attn(1, w.n_q_heads, w.n_kv_heads, w.head_dim, T, dev.cu_seqlens, B, max_seq,
-                        d_rows, d_cur, 0, len(rows), dev.q, dev.k_fresh, dev.v_fresh, kc, vc,
+                        d_rows, d_cur, 0, len(rows), dev.q, dev.k_fresh, dev.v_fresh, kc, vc, None,
                         1.0 / np.sqrt(w.head_dim), kvb.KVB_BF16, out, ws, wsb)
     torch.cuda.synchronize()
     ck, cv = ref.cache_k.copy(), ref.cache_v.copy()
@@ -318,11 +318,11 @@ def test_attention_whole_tile_launch():
     kc, vc = pb.k_cache.clone(), pb.v_cache.clone()
     out = torch.full((L, T, w.n_q_heads, w.head_dim), -1, dtype=torch.int16, device="cuda")
     wsb = kvb.kvb_sparse_attn_workspace_bytes(L, w.n_q_heads, w.n_kv_heads, w.head_dim, T, B, T,
-                                              len(rows))
+                                              len(rows), 0)
     ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
     kvb.kvb_sparse_attn(L, w.n_q_heads, w.n_kv_heads, w.head_dim, T, dev.cu_seqlens, B, T,
                         torch.from_numpy(rows).cuda(), torch.from_numpy(cu_rows).cuda(), 0,
-                        len(rows), dev.q, dev.k_fresh, dev.v_fresh, kc, vc,
+                        len(rows), dev.q, dev.k_fresh, dev.v_fresh, kc, vc, None,
                         1.0 / np.sqrt(w.head_dim), kvb.KVB_BF16, out, ws, wsb)
     torch.cuda.synchronize()
     ck, cv = ref.cache_k.copy(), ref.cache_v.copy()
