@@ -7,9 +7,11 @@
 //
 // Key jobs: one thread takes 4 consecutive tokens (one statistic group,
 // Gk % 4 == 0) and 8 channel pairs (j, j + d/2); statistics and the chunk's
-// rotation row are loaded and widened to double once per job.  Value jobs:
-// one thread takes one token and 16 consecutive channels (one statistic group,
-// Gv % 16 == 0).
+// rotation row are loaded and widened to double once per job.  Value pieces:
+// one thread takes one token and 8 consecutive channels (one statistic group,
+// Gv % 8 == 0; the API asks Gv % 16), so 16 (d = 128) or 8 (d = 64) lanes
+// store a whole row and a wave's stores are contiguous.  Every value input of
+// the thread is loaded before the key work starts, so those loads overlap it.
 //
 // With a non-NULL fp16 shadow the value jobs also store the fp16 image of the
 // bfloat16 values (the operand the attention's P.V product reads).
@@ -39,7 +41,6 @@ stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
   constexpr int CB = D * BITS / 8;       // code bytes per token row
   constexpr int TPT = H / 8;             // key threads per token quad
   constexpr int KJOBS = (kC / 4) * TPT;  // 256 (d=128) or 128 (d=64)
-  constexpr int VJOBS = kC * (D / 16);
   const int c = blockIdx.x;
   const int lh = blockIdx.y;
   const int l = lh / Hkv, h = lh % Hkv;
@@ -51,8 +52,31 @@ stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
   const int64_t out_row0 = ((int64_t)l * Hkv + h) * t_total + ch.dst_row;
   const int ngk = kC / Gk, ngv = D / Gv;
 
-  for (int job = threadIdx.x; job < KJOBS + VJOBS; job += blockDim.x) {
-    if (job < KJOBS) {
+  // value inputs of this thread's pieces (token u, channels [j0, j0 + 8))
+  constexpr int VP = D / 8;              // pieces per token row
+  constexpr int VPT = kC * VP / 256;     // pieces per thread
+  uint32_t vw[VPT][2];
+  float vsc[VPT], vzr[VPT];
+#pragma unroll
+  for (int k = 0; k < VPT; ++k) {
+    const int vj = threadIdx.x + 256 * k;
+    const int u = vj / VP, j0 = (vj % VP) * 8;
+    const int64_t srow = slab * kC + u;
+    vsc[k] = v_scale[srow * ngv + j0 / Gv];
+    vzr[k] = v_zero[srow * ngv + j0 / Gv];
+    const uint8_t* row = v_codes + srow * CB;
+    if constexpr (BITS == 8) {
+      const uint2 a = *reinterpret_cast<const uint2*>(row + j0);
+      vw[k][0] = a.x;
+      vw[k][1] = a.y;
+    } else {
+      vw[k][0] = *reinterpret_cast<const uint32_t*>(row + j0 / 2);
+      vw[k][1] = 0;
+    }
+  }
+
+  for (int job = threadIdx.x; job < KJOBS; job += blockDim.x) {
+    {
       // ---- keys: tokens 4q..4q+3, channel pairs [8cg, 8cg + 8)
       const int q = job / TPT, cg = job % TPT;
       const int u0 = 4 * q, j0 = 8 * cg;
@@ -119,50 +143,30 @@ stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
           *reinterpret_cast<float4*>(ko + H + j0 + 4) = make_float4(yhi[4], yhi[5], yhi[6], yhi[7]);
         }
       }
+    }
+  }
+
+  // ---- values
+#pragma unroll
+  for (int k = 0; k < VPT; ++k) {
+    const int vj = threadIdx.x + 256 * k;
+    const int u = vj / VP, j0 = (vj % VP) * 8;
+    const double sc = vsc[k], zr = vzr[k];
+    float y[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) y[e] = (float)__builtin_fma((double)code_at<BITS>(vw[k], e), sc, zr);
+    const int64_t o = (out_row0 + u) * D + j0;
+    if constexpr (BF16) {
+      const uint4 A = make_uint4(pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]),
+                                 pack_bf16x2(y[4], y[5]), pack_bf16x2(y[6], y[7]));
+      *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(v_out) + o) = A;
+      if (v16_out)  // fp16 image of the bf16 values just written
+        *reinterpret_cast<uint4*>(v16_out + o) = make_uint4(bf16x2_to_f16x2(A.x), bf16x2_to_f16x2(A.y),
+                                                            bf16x2_to_f16x2(A.z), bf16x2_to_f16x2(A.w));
     } else {
-      // ---- values: token u, channels [16vg, 16vg + 16)
-      const int vj = job - KJOBS;
-      const int u = vj / (D / 16), vg = vj % (D / 16);
-      const int j0 = vg * 16;
-      const int64_t srow = slab * kC + u;
-      const double sc = v_scale[srow * ngv + j0 / Gv];
-      const double zr = v_zero[srow * ngv + j0 / Gv];
-      const uint8_t* row = v_codes + srow * CB;
-      uint32_t w[4];
-      if constexpr (BITS == 8) {
-        const uint4 a = *reinterpret_cast<const uint4*>(row + j0);
-        w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
-      } else {
-        const uint2 a = *reinterpret_cast<const uint2*>(row + j0 / 2);
-        w[0] = a.x; w[1] = a.y; w[2] = w[3] = 0;
-      }
-      float y[16];
-#pragma unroll
-      for (int k = 0; k < 16; ++k) y[k] = (float)__builtin_fma((double)code_at<BITS>(w, k), sc, zr);
-      const int64_t o = (out_row0 + u) * D + j0;
-      if constexpr (BF16) {
-        uint16_t* vo = reinterpret_cast<uint16_t*>(v_out) + o;
-        uint4 A, B;
-        A.x = pack_bf16x2(y[0], y[1]);   A.y = pack_bf16x2(y[2], y[3]);
-        A.z = pack_bf16x2(y[4], y[5]);   A.w = pack_bf16x2(y[6], y[7]);
-        B.x = pack_bf16x2(y[8], y[9]);   B.y = pack_bf16x2(y[10], y[11]);
-        B.z = pack_bf16x2(y[12], y[13]); B.w = pack_bf16x2(y[14], y[15]);
-        *reinterpret_cast<uint4*>(vo) = A;
-        *reinterpret_cast<uint4*>(vo + 8) = B;
-        if (v16_out) {
-          // fp16 image of the bf16 values just written
-          uint16_t* ho = v16_out + o;
-          *reinterpret_cast<uint4*>(ho) = make_uint4(bf16x2_to_f16x2(A.x), bf16x2_to_f16x2(A.y),
-                                                     bf16x2_to_f16x2(A.z), bf16x2_to_f16x2(A.w));
-          *reinterpret_cast<uint4*>(ho + 8) = make_uint4(bf16x2_to_f16x2(B.x), bf16x2_to_f16x2(B.y),
-                                                         bf16x2_to_f16x2(B.z), bf16x2_to_f16x2(B.w));
-        }
-      } else {
-        float* vo = reinterpret_cast<float*>(v_out) + o;
-#pragma unroll
-        for (int k = 0; k < 16; k += 4)
-          *reinterpret_cast<float4*>(vo + k) = make_float4(y[k], y[k + 1], y[k + 2], y[k + 3]);
-      }
+      float* vo = reinterpret_cast<float*>(v_out) + o;
+      *reinterpret_cast<float4*>(vo) = make_float4(y[0], y[1], y[2], y[3]);
+      *reinterpret_cast<float4*>(vo + 4) = make_float4(y[4], y[5], y[6], y[7]);
     }
   }
 }
