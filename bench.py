@@ -5,11 +5,15 @@ One step = one pass of the whole path over one 8K-token prompt of the
 KIVI pool with 64 cached chunks at random original offsets, 15 % per-layer
 recompute):
 
-    kvb_stitch (all layers, one launch)
+    kvb_stitch (all layers, one launch; also keeps the fp16 shadow of V)
     kvb_deviation_topk (all layers, one call: deviation + selection)
-    kvb_sparse_attn x 36 (one launch per layer, as a model runs its layers)
+    kvb_sparse_attn x 36 (one call per layer, as a model runs its layers)
 
 Inputs are resident in HBM before the timed region.  Prints one JSON line.
+The roofline object covers the per-layer attention call (the dominant cost):
+algorithmic flops per call / its average duration from HIP events on the
+stream it runs on; "traffic" is the per-call HBM bytes from the committed
+rocprofv3 counter summary when it was taken on the current kernel sources.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--attn-all-layers] [--no-cpu-baseline]
@@ -36,13 +40,18 @@ def log(*a):
 
 
 def algorithmic(w, s, rows_per_set, cu_rows_per_set):
-    """Algorithmic work of one step (bytes a kernel must move, flops it must do)."""
+    """Algorithmic work of one step (bytes a kernel must move, flops it must do).
+
+    Stitch: the codes and statistics it reads, the bf16 K and V rows it writes
+    and the fp16 shadow of V it keeps for the attention.  Deviation: the cache
+    and fresh K rows it reads (bf16) and the deviation it writes.  Attention:
+    4 d Hq flops per (selected query row, visible key): QK^T and PV."""
     L, H, d, C, T, Hq = w.n_layers, w.n_kv_heads, w.head_dim, w.chunk_len, w.t_total, w.n_q_heads
     P = s.n_pool
     cb = d * w.bits // 8
     codes = 2 * P * L * H * C * cb
     stats = P * L * H * (C // w.k_group) * d * 8 + P * L * H * C * (d // w.v_group) * 8
-    stitch_out = 2 * P * L * H * C * d * 2
+    stitch_out = 3 * P * L * H * C * d * 2
     stitch_bytes = codes + stats + stitch_out
     n_sets = rows_per_set.shape[0]
     dev_bytes = 2 * L * H * T * d * 2 + n_sets * T * 4
@@ -53,6 +62,30 @@ def algorithmic(w, s, rows_per_set, cu_rows_per_set):
         r = rows_per_set[si, : cu_rows_per_set[si, -1]]
         flops_per_layer.append(4.0 * d * Hq * float(np.sum(pos[r] + 1)))
     return stitch_bytes, dev_bytes, np.array(flops_per_layer)
+
+
+def committed_traffic(workload):
+    """Per-launch HBM bytes of the attention call from the committed counter
+    summary, if it was taken on the current kernel sources (else None)."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", f"sparse_attn_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None, "no committed counter summary"
+    text = open(path).read()
+    m_b = re.search(r"^traffic_bytes_per_launch:\s*([0-9.eE+]+)", text, re.M)
+    m_h = re.search(r"^kernel_sources_sha256:\s*([0-9a-f]+)", text, re.M)
+    if not (m_b and m_h):
+        return None, "summary lacks the traffic or source-hash line"
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    if h.hexdigest() != m_h.group(1):
+        return None, "attention sources changed since the counters were taken"
+    return float(m_b.group(1)), "rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated"
+
+
+KERNEL_SOURCES = ("paper_2608_21362_amd/csrc/sparse_attn.hip", "paper_2608_21362_amd/csrc/kvb_device.h")
 
 
 def cpu_baseline(w, s, n_layers_sample):
@@ -89,7 +122,8 @@ def main():
     ap.add_argument("--attn-all-layers", action="store_true",
                     help="one attention launch for all layers (ceiling variant)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-layers", type=int, default=20)
+    ap.add_argument("--cpu-layers", type=int, default=24,
+                    help="layers of the oracle timed for cpu_baseline (scaled to the whole step)")
     ap.add_argument("--flush-mb", type=int, default=512)
     ap.add_argument("--calibrate-copy-mb", type=int, default=0,
                     help="also run one plain device copy of this size (counter calibration)")
@@ -194,6 +228,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    traffic, traffic_note = committed_traffic(w.name) if not args.attn_all_layers else (None, "")
     tokens_per_step = w.t_total
     result = {
         "metric": METRIC,
@@ -217,9 +252,10 @@ def main():
             "parallelism": "single GPU",
         },
         "roofline": {
-            "kernel": "kvb_sparse_attn (patch + attention + split combine) per launch",
+            "kernel": "kvb_sparse_attn call per layer (patch, attention and combine kernels)",
             "bound": "mfma", "achieved": attn_tflops, "peak": MFMA_BF16_PEAK_TFLOPS,
-            "unit": "TFLOP/s", "frac": attn_tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": None,
+            "unit": "TFLOP/s", "frac": attn_tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": traffic,
+            "traffic_note": traffic_note,
             "flops_per_launch": attn_flops_launch, "ms_per_launch": attn_ms_launch,
         },
         "kernels": {
