@@ -11,7 +11,7 @@ Readings:
 * candidates are the rows of cached (hit) chunks; n_b counts the candidates of
   prompt b and k_b = floor(rho * n_b) with rho = rho_num / rho_den in integers;
 * order is deviation descending, then row ascending (the lower row wins a
-  tie); -0.0 equals +0.0; NaN ranks below every number;
+  tie); -0.0 equals +0.0; NaN ranks below every number, -inf included;
 * the decision is taken on the float32 value of the deviation;
 * seams are the chunk starts p > 0 of a prompt (sink rows count as content
   before the first chunk); the window of a seam is rows
@@ -53,12 +53,14 @@ def k_per_prompt(cu_seqlens, candidate, rho_num: int, rho_den: int) -> np.ndarra
 
 
 def _rank_key(value: float, row: int):
+    """Sort key: numbers by value descending (-0 as +0), then NaN; row ascending
+    within equal keys."""
     v = float(value)
     if math.isnan(v):
-        v = -math.inf
+        return (1, 0.0, row)
     if v == 0.0:
         v = 0.0
-    return (-v, row)
+    return (0, -v, row)
 
 
 def top_k(delta32, rows, k: int):

@@ -212,8 +212,9 @@ def test_patch_and_attention(name):
 
 
 def test_select_stage_isolated_with_ties():
-    """Selection alone on generator-drawn deviations with exact ties, -0/+0
-    and several prompts and sets: bit-exact with the oracle."""
+    """Selection alone on generator-drawn deviations with exact ties, -0/+0,
+    planted non-finite values and several prompts and sets: bit-exact with the
+    oracle."""
     _need_gpu()
     from paper_2608_21362_amd import kvb
 
@@ -228,6 +229,11 @@ def test_select_stage_isolated_with_ties():
     flags[forced] |= 2
     for levels in (0, 5, 40):
         delta = kw.deviation_draw(n_sets, T, seed=levels, n_levels=levels)
+        if levels == 5:  # NaN ranks below every number (-inf included), +inf first
+            spots = np.random.default_rng(77).choice(T, size=(3, 40), replace=False)
+            delta[:, spots[0]] = np.nan
+            delta[:, spots[1]] = -np.inf
+            delta[:, spots[2]] = np.inf
         ks = []
         for si in range(n_sets):
             kk = osel.k_per_prompt(cu, cand, 15 + 10 * si, 100)

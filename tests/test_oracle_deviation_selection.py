@@ -101,6 +101,12 @@ def test_lower_row_wins_ties_and_signed_zero():
     assert selection.top_k(d, [7, 6, 5], 2) == [5, 6]        # -0 ties +0, lower row first
 
 
+def test_nan_ranks_below_every_number():
+    d = np.array([np.nan, -np.inf, 0.25, np.nan, np.inf, -1.0], np.float32)
+    assert selection.top_k(d, range(6), 6) == [4, 2, 5, 1, 0, 3]
+    assert selection.top_k(d, range(6), 4) == [4, 2, 5, 1]
+
+
 def test_k_zero_and_k_all():
     T = 300
     cu = np.array([0, T], np.int32)
