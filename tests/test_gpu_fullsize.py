@@ -1,0 +1,134 @@
+"""Full-size GPU parity: the 36-layer 8K workload on every layer, the batched
+16 x 2048 workload, and three layers of the 36-layer 32K workload at their
+full per-layer size, in the launch configuration bench.py times (one stitch
+and one deviation + selection for all populated layers, then one attention
+call per layer with the fp16 shadow of V).
+
+Checks per layer, against the oracle built from the same seeded draws:
+stitch bit-exact (K, V and the fp16 shadow of the stitched V), deviation
+within 1 fp32 ulp, selection by the margin / band rule, patch bit-exact on the
+GPU's own row set, the shadow equal to the fp16 image of the final V cache,
+and attention within |o - o_ref| <= 2e-2 + 1e-2 |o_ref| on a stratified sample
+of selected rows (every selected row on the first and last layer of the 8K
+workload).  The oracle is evaluated one layer at a time.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import kvb_workload as kw
+from oracle import attention as oatt
+from oracle import deviation as odev
+from oracle import numerics, populate as opop, selection as osel, stitch as ostitch
+
+ATOL, RTOL = 2e-2, 1e-2
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _np16(t):
+    return t.detach().cpu().numpy().view(np.uint16)
+
+
+def _f16_of_bf16(bits):
+    """fp16 bit patterns of bf16 values (numpy's float32 -> float16, RNE)."""
+    return numerics.bf16_bits_to_f32(bits).astype(np.float16).view(np.uint16)
+
+
+def _ulp32(x):
+    return np.spacing(np.abs(np.asarray(x, np.float32)))
+
+
+CASES = [
+    # name, GPU-populated layers (None = all), attention sample per layer, full layers
+    ("qwen_36l_8k", None, 256, "ends"),
+    ("batched_mixed", None, 1024, ""),
+    ("long_32k", [0, 17, 35], 256, ""),
+]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name,layers,n_sample,full", CASES, ids=[c[0] for c in CASES])
+def test_fullsize(name, layers, n_sample, full):
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2608_21362_amd import pipeline
+
+    w = kw.WORKLOADS[name]
+    s = kw.structure(w)
+    gl = list(range(w.n_layers)) if layers is None else list(layers)
+    L, T = len(gl), w.t_total
+    _say(f"[fullsize] {name}: layers {gl[0]}..{gl[-1]} ({L}) T={T}")
+    dev = pipeline.populate(w, s, layers=gl)
+    pb = pipeline.buffers(dev)
+    pipeline.stitch(dev, pb)
+    st_k, st_v, st_v16 = pb.k_cache.clone(), pb.v_cache.clone(), pb.v_cache_f16.clone()
+    pipeline.deviation_topk(dev, pb)
+    for i in range(L):
+        pipeline.sparse_attn_layer(dev, pb, i)
+    torch.cuda.synchronize()
+    _say(f"[fullsize] {name}: GPU path done")
+    rows_all = pb.rows.cpu().numpy()
+    cu_all = pb.cu_rows.cpu().numpy()
+    delta = pb.delta.cpu().numpy()
+    forced = osel.forced_rows(s.cu_seqlens, s.hit_row, s.chunk_starts, w.seam_left, w.seam_right)
+    kseq = osel.k_per_prompt(s.cu_seqlens, s.hit_row, w.rho_num, w.rho_den)
+    hit = s.hit_row
+    rng = np.random.default_rng(9)
+    worst = 0.0
+    for i, l in enumerate(gl):
+        ref = opop.populate(w, s, layers=[l])
+        ck, cv = ref.cache_k.copy(), ref.cache_v.copy()
+        ostitch.stitch_into(ck, cv, ref.pool, ref.chunks, ref.cos, ref.sin, "bf16")
+        # stitch (before the patch), with the fp16 shadow of the stitched V rows
+        gk0, gv0, gh0 = _np16(st_k[i]), _np16(st_v[i]), _np16(st_v16[i])
+        assert np.array_equal(gk0, ck[0]), f"layer {l}: stitched K"
+        assert np.array_equal(gv0, cv[0]), f"layer {l}: stitched V"
+        assert np.array_equal(gh0[:, hit], _f16_of_bf16(cv[0][:, hit])), f"layer {l}: fp16 shadow"
+        # deviation
+        rd32 = odev.deviation(ck, ref.k_fresh, per_layer=True)[0].astype(np.float32)
+        gd = delta[i]
+        assert np.all(np.abs(gd.astype(np.float64) - rd32) <= _ulp32(rd32)), f"layer {l}: deviation"
+        # selection: equal, or differing only inside the 1e-4 band at the cut
+        g_rows = rows_all[i, : cu_all[i, -1]]
+        r_rows, r_cu = osel.select(rd32, hit, forced, s.cu_seqlens, kseq)
+        assert np.all(np.diff(g_rows) > 0)
+        if not (np.array_equal(g_rows, r_rows) and np.array_equal(cu_all[i], r_cu)):
+            diff = np.setxor1d(g_rows, r_rows)
+            for b in range(len(s.cu_seqlens) - 1):
+                lo, hi = s.cu_seqlens[b], s.cu_seqlens[b + 1]
+                cand = [r for r in range(lo, hi) if hit[r]]
+                order = osel.top_k(rd32, cand, len(cand))
+                k = int(kseq[b])
+                d_b = diff[(diff >= lo) & (diff < hi)]
+                if len(d_b) and 0 < k < len(order):
+                    kth = float(rd32[order[k - 1]])
+                    assert np.all(np.abs(rd32[d_b].astype(np.float64) - kth) <= 1e-4), \
+                        f"layer {l}: selection differs outside the margin band"
+            _say(f"[fullsize] {name} layer {l}: {len(diff)} rows differ inside the band")
+        # patch on the GPU's rows; the shadow is the fp16 image of the final V
+        pk = oatt.patch(ck[0], ref.k_fresh[0], g_rows)
+        pv = oatt.patch(cv[0], ref.v_fresh[0], g_rows)
+        gk, gv, gh = _np16(pb.k_cache[i]), _np16(pb.v_cache[i]), _np16(pb.v_cache_f16[i])
+        assert np.array_equal(gk, pk) and np.array_equal(gv, pv), f"layer {l}: patch"
+        assert np.array_equal(gh, _f16_of_bf16(gv)), f"layer {l}: fp16 shadow after the patch"
+        # attention
+        if full == "ends" and i in (0, L - 1):
+            sample = g_rows
+        else:
+            sample = np.sort(rng.choice(g_rows, size=min(n_sample, len(g_rows)), replace=False))
+        refo = oatt.attend_rows(ref.q[0], pk, pv, sample, s.cu_seqlens)
+        idx = torch.from_numpy(sample.astype(np.int64)).cuda()
+        got = numerics.bf16_bits_to_f32(_np16(pb.out[i].index_select(0, idx))).astype(np.float64)
+        err = np.abs(got - refo)
+        ratio = float(np.max(err / (ATOL + RTOL * np.abs(refo))))
+        worst = max(worst, ratio)
+        assert ratio <= 1.0, f"layer {l}: attention error/tolerance {ratio:.3f}"
+        if i in (0, L - 1) or i % 8 == 0:
+            _say(f"[fullsize] {name} layer {l}: rows {len(g_rows)} sampled {len(sample)} "
+                 f"max|err| {err.max():.3e} max err/tol {ratio:.3f}")
+    _say(f"[fullsize] {name}: worst attention err/tol {worst:.3f}")
