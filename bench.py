@@ -198,17 +198,22 @@ def main():
     attn_flops_launch = float(flops.mean()) if not args.attn_all_layers else float(flops.sum())
     attn_tflops = attn_flops_launch / (attn_ms_launch * 1e-3) / 1e12
 
-    # stitch and deviation bandwidth with the 256 MiB Infinity Cache flushed between reps
-    flush = torch.empty(args.flush_mb << 20, dtype=torch.uint8, device="cuda")
+    # stitch and deviation bandwidth with the 256 MiB Infinity Cache flushed
+    # between reps: a read of a larger buffer leaves only clean lines, so the
+    # timed call neither hits its inputs in the cache nor pays for another
+    # kernel's write-back
+    flush = torch.ones(args.flush_mb << 18, dtype=torch.float32, device="cuda")
     st_f, dv_f = [], []
     for _ in range(5):
-        flush.fill_(1)
+        flush.sum()
+        torch.cuda.synchronize()
         a, b, c = ev(), ev(), ev()
         a.record(stream)
         pipeline.stitch(di, pb)
         b.record(stream)
         torch.cuda.synchronize()
-        flush.fill_(2)
+        flush.sum()
+        torch.cuda.synchronize()
         b2 = ev()
         b2.record(stream)
         pipeline.deviation_topk(di, pb)

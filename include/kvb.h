@@ -187,7 +187,8 @@ kvb_status kvb_stitch(const kvb_pool_layout* pool, int32_t n_pool,
  * over the bf16 inputs; when |a|^2 |b|^2 == 0 it is 1 if both vectors are zero
  * and 0 otherwise.  delta: f32 [per_layer ? L : 1][t_total] (the double rounded
  * once).  Inputs bf16 [L][Hkv][t_total][d].
- * Errors: KVB_EINVAL (incl. exactly one V pointer NULL), KVB_EUNSUPPORTED (d). */
+ * Errors: KVB_EINVAL (incl. exactly one V pointer NULL), KVB_EUNSUPPORTED (d not
+ * 64/128, Hkv not a power of two up to 16). */
 kvb_status kvb_deviation(int32_t n_layers, int32_t n_kv_heads, int32_t head_dim, int64_t t_total,
                          const uint16_t* k_cache, const uint16_t* k_fresh,
                          const uint16_t* v_cache, const uint16_t* v_fresh,

@@ -217,6 +217,8 @@ static kvb_status check_deviation(int32_t n_layers, int32_t n_kv_heads, int32_t 
                                   const uint16_t* v_fresh, float* delta) {
   if (kvb_status s = check_head_dim(head_dim)) return s;
   REQUIRE(n_layers > 0 && n_kv_heads > 0, "n_layers and n_kv_heads must be positive");
+  if (n_kv_heads > 16 || (n_kv_heads & (n_kv_heads - 1)))
+    return fail(KVB_EUNSUPPORTED, "n_kv_heads %d: must be a power of two up to 16", n_kv_heads);
   REQUIRE(t_total > 0 && t_total <= INT32_MAX, "t_total must be in (0, 2^31)");
   REQUIRE((v_cache == nullptr) == (v_fresh == nullptr), "give both value tensors or neither");
   const void* ptrs[] = {k_cache, k_fresh, delta};

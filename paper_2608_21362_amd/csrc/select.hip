@@ -10,6 +10,12 @@
 // output is ascending without a sort and no atomic decides an order.  LDS
 // atomics only count histogram bins.
 //
+// Segments of up to 48K rows use select_reg_kernel: every thread keeps the keys
+// and flags of its KPT rows (rows lo + j * 1024 + tid) in registers, so the
+// four histogram passes touch no memory but LDS, and the compaction takes one
+// ballot per register slot with a single block-wide prefix over all of them.
+// Longer segments use select_kernel, which re-reads the keys on every pass.
+//
 // Several prompts per set: rows go to a staging area at the prompt's own row
 // offset and a second small kernel packs them and writes cu_rows.
 #include "kvb_device.h"
@@ -179,6 +185,207 @@ select_kernel(int64_t t_total, const int32_t* __restrict__ cu_seqlens, int32_t n
   (void)lane;
 }
 
+
+// Radix select of the k-th largest key among the candidate keys of this
+// thread's register slots; every thread must call.  Returns tau and how many
+// candidates equal to tau are still needed.
+template <int KPT>
+__device__ __forceinline__ void radix_select_reg(const uint32_t (&key)[KPT], uint64_t candm,
+                                                 uint32_t k, uint32_t* hist, uint32_t* sh_prefix,
+                                                 uint32_t* sh_remaining, uint32_t* tau,
+                                                 uint32_t* need_eq) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  uint32_t prefix = 0, remaining = k;
+  for (int digit = 3; digit >= 0; --digit) {
+    for (int i = tid; i < 256; i += kThreads) hist[i] = 0;
+    __syncthreads();
+    const uint32_t hi_mask = digit == 3 ? 0u : (0xFFFFFFFFu << (8 * (digit + 1)));
+    int run_bin = -1;
+    uint32_t run_n = 0;
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+      if (!((candm >> j) & 1ull)) continue;
+      if ((key[j] & hi_mask) != (prefix & hi_mask)) continue;
+      const int bin = (key[j] >> (8 * digit)) & 0xFF;
+      if (bin == run_bin) {
+        ++run_n;
+      } else {
+        if (run_n) atomicAdd(&hist[run_bin], run_n);
+        run_bin = bin;
+        run_n = 1;
+      }
+    }
+    if (run_n) atomicAdd(&hist[run_bin], run_n);
+    __syncthreads();
+    if (wave == 0) {
+      // lane i owns bins 255-4i .. 252-4i (walking from the top)
+      uint32_t hb[4], sum = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        hb[j] = hist[255 - 4 * lane - j];
+        sum += hb[j];
+      }
+      uint32_t incl = sum;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t v = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += v;
+      }
+      const uint64_t hit = __ballot(incl >= remaining);
+      const int first = __ffsll((unsigned long long)hit) - 1;
+      if (lane == first) {
+        uint32_t cum = incl - sum;
+        for (int j = 0; j < 4; ++j) {
+          if (cum + hb[j] >= remaining) {
+            *sh_prefix = prefix | ((uint32_t)(255 - 4 * lane - j) << (8 * digit));
+            *sh_remaining = remaining - cum;
+            break;
+          }
+          cum += hb[j];
+        }
+      }
+    }
+    __syncthreads();
+    prefix = *sh_prefix;
+    remaining = *sh_remaining;
+  }
+  *tau = prefix;
+  *need_eq = remaining;
+}
+
+// Per-slot, per-wave counts of a bit (slot-major, then thread order) into
+// wcnt; returns the block-wide total.  Every thread must call; wcnt is valid
+// until the next call.
+template <int KPT>
+__device__ __forceinline__ uint32_t slot_counts(uint64_t bits, uint32_t (*wcnt)[kWaves],
+                                                int nslots) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();  // the previous user of wcnt is done
+#pragma unroll
+  for (int j = 0; j < KPT; ++j) {
+    if (j < nslots) {
+      const uint64_t ball = __ballot((bits >> j) & 1ull);
+      if (lane == 0) wcnt[j][wave] = (uint32_t)__popcll(ball);
+    }
+  }
+  __syncthreads();
+  uint32_t tot = 0;
+  for (int j = 0; j < nslots; ++j)
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) tot += wcnt[j][w];
+  return tot;
+}
+
+// Exclusive rank of slot j's bit among all set bits (slot-major, then thread),
+// from the counts of slot_counts and the running total of slots before j.
+__device__ __forceinline__ uint32_t slot_rank(uint64_t bits, int j, const uint32_t (*wcnt)[kWaves],
+                                              uint32_t run_before, uint32_t* slot_total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t ball = __ballot((bits >> j) & 1ull);
+  uint32_t before = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const uint32_t c = wcnt[j][w];
+    before += (w < wave) ? c : 0u;
+    tot += c;
+  }
+  *slot_total = tot;
+  return run_before + before + (uint32_t)__popcll(ball & ((1ull << lane) - 1ull));
+}
+
+template <int KPT>
+__global__ void __launch_bounds__(kThreads)
+select_reg_kernel(int64_t t_total, const int32_t* __restrict__ cu_seqlens, int32_t n_seqs,
+                  const float* __restrict__ delta, const uint8_t* __restrict__ flags,
+                  const int32_t* __restrict__ k_per_seq, int32_t* __restrict__ rows_out,
+                  int32_t* __restrict__ cu_rows, int32_t* __restrict__ staging,
+                  int32_t* __restrict__ counts) {
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t wcnt[KPT][kWaves];
+  __shared__ uint32_t sh_prefix, sh_remaining;
+  const int b = blockIdx.x;
+  const int64_t set = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int64_t lo = cu_seqlens[b], hi = cu_seqlens[b + 1];
+  const int nslots = (int)((hi - lo + kThreads - 1) / kThreads);  // <= KPT by the launch
+  const float* dl = delta + set * t_total;
+
+  // this thread's rows lo + j * kThreads + tid: keys and flags, loaded once
+  uint32_t key[KPT];
+  uint64_t candm = 0, forcedm = 0;
+#pragma unroll
+  for (int j = 0; j < KPT; ++j) {
+    key[j] = 0;
+    const int64_t r = lo + (int64_t)j * kThreads + tid;
+    if (j < nslots && r < hi) {
+      const uint32_t f = flags[r];
+      if (f & KVB_ROW_CANDIDATE) {
+        candm |= 1ull << j;
+        key[j] = order_key(dl[r]);
+      }
+      if (f & KVB_ROW_FORCED) forcedm |= 1ull << j;
+    }
+  }
+  const uint32_t n_cand = slot_counts<KPT>(candm, wcnt, nslots);
+  int64_t k = k_per_seq[set * n_seqs + b];
+  if (k < 0) k = 0;
+  const bool take_all = k >= (int64_t)n_cand;
+  const bool take_none = k == 0;
+
+  uint64_t gtm = 0, eqm = 0;
+  if (take_all) {
+    gtm = candm;
+  } else if (!take_none) {
+    uint32_t tau, need_eq;
+    radix_select_reg<KPT>(key, candm, (uint32_t)k, hist, &sh_prefix, &sh_remaining, &tau,
+                          &need_eq);
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+      if ((candm >> j) & 1ull) {
+        if (key[j] > tau) gtm |= 1ull << j;
+        if (key[j] == tau) eqm |= 1ull << j;
+      }
+    }
+    // the first need_eq keys equal to tau, in row order (the lower row wins a tie)
+    const uint32_t n_eq = slot_counts<KPT>(eqm, wcnt, nslots);
+    if (need_eq < n_eq) {
+      uint32_t run = 0;
+      uint64_t keep = 0;
+#pragma unroll
+      for (int j = 0; j < KPT; ++j) {
+        if (j < nslots) {
+          uint32_t tot;
+          const uint32_t rk = slot_rank(eqm, j, wcnt, run, &tot);
+          if (((eqm >> j) & 1ull) && rk < need_eq) keep |= 1ull << j;
+          run += tot;
+        }
+      }
+      eqm = keep;
+    }
+  }
+  const uint64_t selm = forcedm | gtm | eqm;
+  const uint32_t n_sel = slot_counts<KPT>(selm, wcnt, nslots);
+  int32_t* dst = (n_seqs == 1) ? rows_out + set * t_total : staging + set * t_total + lo;
+  uint32_t run = 0;
+#pragma unroll
+  for (int j = 0; j < KPT; ++j) {
+    if (j < nslots) {
+      uint32_t tot;
+      const uint32_t rk = slot_rank(selm, j, wcnt, run, &tot);
+      if ((selm >> j) & 1ull) dst[rk] = (int32_t)(lo + (int64_t)j * kThreads + tid);
+      run += tot;
+    }
+  }
+  if (tid == 0) {
+    if (n_seqs == 1) {
+      cu_rows[set * 2] = 0;
+      cu_rows[set * 2 + 1] = (int32_t)n_sel;
+    } else {
+      counts[set * n_seqs + b] = (int32_t)n_sel;
+    }
+  }
+}
+
 __global__ void __launch_bounds__(256)
 pack_kernel(int64_t t_total, const int32_t* __restrict__ cu_seqlens, int32_t n_seqs,
             const int32_t* __restrict__ staging, const int32_t* __restrict__ counts,
@@ -224,9 +431,23 @@ hipError_t launch_select(int32_t n_sets, int64_t t_total, const int32_t* cu_seql
     const size_t st = (size_t)n_sets * (size_t)t_total * sizeof(int32_t);
     counts = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(workspace) + ((st + 255) / 256) * 256);
   }
-  hipLaunchKernelGGL(select_kernel, dim3(n_seqs, n_sets), dim3(kThreads), 0, s, t_total,
-                     cu_seqlens, n_seqs, delta, row_flags, k_per_seq, rows, cu_rows, staging,
-                     counts);
+  // the longest prompt is at most t_total rows: pick the register-slot count from it
+  const dim3 grid(n_seqs, n_sets);
+#define KVB_SELECT_REG(K)                                                                       \
+  hipLaunchKernelGGL(select_reg_kernel<K>, grid, dim3(kThreads), 0, s, t_total, cu_seqlens,     \
+                     n_seqs, delta, row_flags, k_per_seq, rows, cu_rows, staging, counts)
+  if (t_total <= 8 * kThreads)
+    KVB_SELECT_REG(8);
+  else if (t_total <= 16 * kThreads)
+    KVB_SELECT_REG(16);
+  else if (t_total <= 32 * kThreads)
+    KVB_SELECT_REG(32);
+  else if (t_total <= 48 * kThreads)
+    KVB_SELECT_REG(48);
+  else
+    hipLaunchKernelGGL(select_kernel, grid, dim3(kThreads), 0, s, t_total, cu_seqlens, n_seqs,
+                       delta, row_flags, k_per_seq, rows, cu_rows, staging, counts);
+#undef KVB_SELECT_REG
   if (n_seqs > 1)
     hipLaunchKernelGGL(pack_kernel, dim3(n_seqs, n_sets), dim3(256), 0, s, t_total, cu_seqlens,
                        n_seqs, staging, counts, rows, cu_rows);

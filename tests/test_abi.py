@@ -127,6 +127,8 @@ def _dev_args(**over):
 @pytest.mark.parametrize("over,status", [
     (dict(v_cache=FAKE), kvb.KVB_EINVAL),            # exactly one value tensor
     (dict(head_dim=80), kvb.KVB_EUNSUPPORTED),
+    (dict(n_kv_heads=3), kvb.KVB_EUNSUPPORTED),
+    (dict(n_kv_heads=32), kvb.KVB_EUNSUPPORTED),
     (dict(n_layers=0), kvb.KVB_EINVAL),
     (dict(k_fresh=None), kvb.KVB_EINVAL),
     (dict(delta=FAKE + 8), kvb.KVB_EINVAL),
