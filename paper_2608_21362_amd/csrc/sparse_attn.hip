@@ -76,6 +76,20 @@ constexpr int kQT = kQW * kWaves;       // query vectors per workgroup
 constexpr int kKB = 32;                 // keys per block = one 32-row MFMA tile
 constexpr int kStages = 4;              // LDS ring depth (blocks in flight: 2 ahead)
 constexpr int kAttnMaxWorkgroups = 1024;  // attention workgroups (sizes the partial records)
+// Balanced ranges charge every tile a fixed cost, in 32-key block units, for a
+// segment's start (tile rows, queries and the first blocks fetched) and end
+// (output or partial record written), so that workgroups covering many short
+// tiles get fewer blocks.  Measured on MI355X at 8K keys per prompt: a
+// segment's start and end take as long as five to eight blocks, and 7 gave
+// the shortest per-layer launches of the values tried (0, 2, 4, 7).
+constexpr int kSegCost = 7;
+// With two workgroups per CU the dispatcher gives workgroups 0 .. CUs-1 the
+// first slot of every CU and the rest the second; the hardware issues the
+// older (first) workgroup's waves first, so it progresses about 1.4 times
+// faster while both run.  Balanced ranges give first-slot workgroups 7/5 of the
+// units of second-slot ones so that the two finish together (measured; a
+// different placement only costs balance, never correctness).
+constexpr int kFirstShareNum = 7, kFirstShareDen = 5;
 constexpr float kLazy = 8.0f;           // max growth (log2 units) tolerated before a rescale
 
 #define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
@@ -113,6 +127,14 @@ struct Tile {
   int b;          // prompt
   int r_begin;    // first entry of the tile in the set's row list
   int r_end;
+};
+
+// What a segment needs to know about its tile.
+struct SegTile {
+  int lg;               // layer * Hkv + kv head
+  int r_begin, r_end;   // entries of the tile in the set's row list
+  int kstart;           // first key (row) of the tile's prompt
+  int kend;             // one past the tile's last query row
 };
 
 __device__ __forceinline__ bool find_tile(const int32_t* cur, int n_seqs, int rows_per_tile,
@@ -363,31 +385,23 @@ __host__ __device__ constexpr int64_t rec_ml_offset(int64_t n_rec) {
 // One segment: key blocks [blk_lo, blk_hi) (32 keys each, counted from the
 // tile's prompt start) of one tile of selected rows of (layer, kv head).  With
 // rec < 0 the segment covers the whole tile and writes the normalised output;
-// otherwise it writes partial record `rec` (unnormalised O, running maximum in
-// log2 units, running sum) for the combine pass.
+// otherwise it writes partial record `rec` (O normalised by this segment's
+// sum, running maximum in log2 units, running sum) for the combine pass.
 template <int D>
 __device__ __forceinline__ void attend_segment(
-    int lg, int slot, int blk_lo, int blk_hi, int rec, int n_rec, char* k_ring, char* v_ring,
-    int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total, const int32_t* __restrict__ cu_seqlens,
-    int32_t n_seqs, const int32_t* __restrict__ rows, const int32_t* __restrict__ cu_rows,
-    int32_t rows_per_layer, int32_t rows_per_tile, const uint16_t* __restrict__ q,
-    const uint16_t* __restrict__ kc, const uint16_t* __restrict__ v16, float c_log2,
-    int32_t out_f32, void* __restrict__ out, float* __restrict__ parts) {
+    const SegTile& tl, int blk_lo, int blk_hi, int rec, int n_rec, char* k_ring, char* v_ring,
+    int32_t Hq, int32_t Hkv, int32_t log2g, int64_t t_total, const int32_t* __restrict__ rows,
+    int32_t rows_per_layer, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
+    const uint16_t* __restrict__ v16, float c_log2, int32_t out_f32, void* __restrict__ out,
+    float* __restrict__ parts) {
   using C = AttnCfg<D>;
   const int G = 1 << log2g;
-  const int l = lg / Hkv, g = lg % Hkv;
-  const int64_t set = rows_per_layer ? l : 0;
-  const int32_t* cur = cu_rows + set * (n_seqs + 1);
-  const int32_t* rws = rows + set * t_total;
-  Tile tile;
-  if (!find_tile(cur, n_seqs, rows_per_tile, slot, &tile)) return;
+  const int l = tl.lg / Hkv, g = tl.lg % Hkv;
+  const int32_t* rws = rows + (rows_per_layer ? (int64_t)l : 0) * t_total;
   const int T = (int)t_total;
-  const int kstart = cu_seqlens[tile.b];
-  const int kend = min(rws[tile.r_end - 1] + 1, T);
-  const int k_lo = kstart + blk_lo * kKB;
-  const int k_hi = min(kstart + blk_hi * kKB, kend);
+  const int k_lo = tl.kstart + blk_lo * kKB;
+  const int k_hi = min(tl.kstart + blk_hi * kKB, tl.kend);
   if (k_hi <= k_lo) return;
-  const int t_min = rws[tile.r_begin];
 
   // the previous segment of this workgroup is done with the LDS ring
   wait_lgkmcnt0();
@@ -398,11 +412,12 @@ __device__ __forceinline__ void attend_segment(
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5, n = lane & 31;
   const int rows_per_wave = kQW >> log2g;
-  const int row_idx = tile.r_begin + wave * rows_per_wave + (n >> log2g);
+  const int row_idx = tl.r_begin + wave * rows_per_wave + (n >> log2g);
   const int head = g * G + (n & (G - 1));
-  int t_q = row_idx < tile.r_end ? rws[row_idx] : -1;
-  const bool qvalid = t_q >= kstart && t_q < kend;  // rows outside the prompt are skipped
-  if (!qvalid) t_q = -1;
+  // this lane's query row, and the smallest query row of this wave (rows are
+  // ascending within a tile): blocks wholly at or below it need no mask
+  int t_q = row_idx < tl.r_end ? rws[row_idx] : -1;
+  const int t_min = rws[min(tl.r_begin + wave * rows_per_wave, tl.r_end - 1)];
 
   const int64_t kv_base = ((int64_t)l * Hkv + g) * t_total * D;
   const i32x4 krs = buffer_rsrc(kc + kv_base, T * C::ROWB);
@@ -413,8 +428,14 @@ __device__ __forceinline__ void attend_segment(
   auto kst = [&](int b) { return k_ring + (b & 3) * C::BLK; };  // ring stage of block b
   auto vst = [&](int b) { return v_ring + (b & 3) * C::BLK; };
 
+  // The first three blocks depend only on the tile: they are requested while
+  // the query rows are on their way.
   issue_block<D>(krs, vrs, k_lo, lo, kst(0), vst(0), wave);
+  if (nblk > 1) issue_block<D>(krs, vrs, k_lo + kKB, lo, kst(1), vst(1), wave);
+  if (nblk > 2) issue_block<D>(krs, vrs, k_lo + 2 * kKB, lo, kst(2), vst(2), wave);
 
+  const bool qvalid = t_q >= tl.kstart && t_q < tl.kend;  // rows outside the prompt are skipped
+  if (!qvalid) t_q = -1;
   // Q^T operand: query n, d = (D/2) h + 8 s + v
   bf16x8 qop[C::NS];
   {
@@ -426,11 +447,9 @@ __device__ __forceinline__ void attend_segment(
       qop[s] = __builtin_bit_cast(bf16x8, w);
     }
   }
-  // Q and block 0 land before anything else is issued: the compiler then never
+  // Queries and the first blocks land before the loop: the compiler then never
   // waits on the queries -- and so on the in-flight prefetch -- later on.
   wait_vmcnt<0>();
-  if (nblk > 1) issue_block<D>(krs, vrs, k_lo + kKB, lo, kst(1), vst(1), wave);
-  if (nblk > 2) issue_block<D>(krs, vrs, k_lo + 2 * kKB, lo, kst(2), vst(2), wave);
   __builtin_amdgcn_s_barrier();
   compiler_fence();
 
@@ -517,29 +536,46 @@ __device__ __forceinline__ void attend_segment(
   }
 }
 
-// int32 offset of the per-tile metadata inside the plan area
+// Plan area (int32): [0] c1, [1] c2, [2] n_first, [3] total, [4 .. 4+n_tiles]
+// prefix, [5+n_tiles ..) first tile of every workgroup, then the per-tile
+// metadata (int4) at this offset.
 __host__ __device__ constexpr int64_t tile_meta_offset(int64_t n_tiles, int64_t n_wg_max) {
-  return ((3 + n_tiles + n_wg_max + 3) / 4) * 4;
+  return ((5 + n_tiles + n_wg_max + 3) / 4) * 4;
 }
 
-// Work decomposition.  Work unit = one 32-key block of one tile; units are
-// numbered tile by tile (tile index = (layer x kv head) * tile_slots + slot).
-// One workgroup builds the exclusive prefix sum of the tiles' block counts,
-// then every attention workgroup w takes the contiguous units [w C, (w+1) C)
-// with C = ceil(total / n_wg), so all workgroups get the same work.
-//   plan[0] = C, plan[1] = total, plan[2 .. 2+n_tiles] = prefix,
-//   plan[3+n_tiles .. 3+n_tiles+n_wg) = tile holding unit w C,
+// First unit of workgroup w: the first n_first workgroups take c1 units each,
+// the others c2.
+__device__ __forceinline__ int unit_start(int w, int c1, int c2, int nf) {
+  return w < nf ? w * c1 : nf * c1 + (w - nf) * c2;
+}
+
+// Workgroup whose range holds unit u.
+__device__ __forceinline__ int unit_owner(int u, int c1, int c2, int nf) {
+  const int b = nf * c1;
+  return u < b ? u / c1 : nf + (u - b) / c2;
+}
+
+// Work decomposition.  Work unit = one 32-key block of one tile, and a tile
+// with blocks also counts kSegCost units for its fixed cost (they come first
+// and hold no blocks); units are numbered tile by tile (tile index =
+// (layer x kv head) * tile_slots + slot).  One workgroup builds the exclusive
+// prefix sum of the tiles' unit counts, then attention workgroup w takes the
+// contiguous units [unit_start(w), unit_start(w + 1)): c1 units for each of the
+// first n_first workgroups, c2 for the others, sized to cover every unit.
+//   plan[0] = c1, plan[1] = c2, plan[2] = n_first, plan[3] = total,
+//   plan[4 .. 4+n_tiles] = prefix,
+//   plan[5+n_tiles .. 5+n_tiles+n_wg) = tile holding unit unit_start(w),
 //   then per tile an int4 {first row entry, end row entry, key start, key end}
 //   at the 16-byte aligned offset tile_meta_offset(n_tiles, n_wg_max).
 __device__ __forceinline__ void build_plan(
     int32_t n_tiles, int32_t tile_slots, int32_t Hkv, int64_t t_total,
     const int32_t* __restrict__ cu_seqlens, int32_t n_seqs, const int32_t* __restrict__ rows,
     const int32_t* __restrict__ cu_rows, int32_t rows_per_layer, int32_t rows_per_tile,
-    int32_t n_wg, int32_t n_wg_max, int32_t* __restrict__ plan) {
+    int32_t n_wg, int32_t n_first, int32_t n_wg_max, int32_t* __restrict__ plan) {
   __shared__ int warp_sums[16];
   __shared__ int carry_sh;
-  int32_t* prefix = plan + 2;
-  int32_t* first = plan + 3 + n_tiles;
+  int32_t* prefix = plan + 4;
+  int32_t* first = plan + 5 + n_tiles;
   int4* meta = reinterpret_cast<int4*>(plan + tile_meta_offset(n_tiles, n_wg_max));
   const int nt = blockDim.x;  // a multiple of 64, at most 1024
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -557,7 +593,7 @@ __device__ __forceinline__ void build_plan(
       if (find_tile(cur, n_seqs, rows_per_tile, slot, &tile)) {
         const int64_t kstart = cu_seqlens[tile.b];
         const int64_t kend = min((int64_t)rows[set * t_total + tile.r_end - 1] + 1, t_total);
-        if (kend > kstart) nb = (int)((kend - kstart + kKB - 1) / kKB);
+        if (kend > kstart) nb = (int)((kend - kstart + kKB - 1) / kKB) + kSegCost;
         mt = make_int4(tile.r_begin, tile.r_end, (int)kstart, (int)kend);
       }
       meta[t] = mt;
@@ -579,16 +615,21 @@ __device__ __forceinline__ void build_plan(
     __syncthreads();
   }
   const int total = carry_sh;
-  const int chunk = max(1, (total + n_wg - 1) / n_wg);
+  // n_first c1 + (n_wg - n_first) c2 >= total with c1 / c2 >= kFirstShareNum / kFirstShareDen
+  const int64_t weight = (int64_t)kFirstShareNum * n_first + (int64_t)kFirstShareDen * (n_wg - n_first);
+  const int c2 = (int)max((int64_t)1, ((int64_t)kFirstShareDen * total + weight - 1) / weight);
+  const int c1 = (int)(((int64_t)kFirstShareNum * c2 + kFirstShareDen - 1) / kFirstShareDen);
   if (tid == 0) {
-    plan[0] = chunk;
-    plan[1] = total;
+    plan[0] = c1;
+    plan[1] = c2;
+    plan[2] = n_first;
+    plan[3] = total;
     prefix[n_tiles] = total;
   }
   __syncthreads();
-  // tile holding unit w * chunk: the largest t with prefix[t] <= w * chunk
+  // tile holding unit unit_start(w): the largest t with prefix[t] <= unit_start(w)
   for (int w = tid; w < n_wg; w += nt) {
-    const int u = w * chunk;
+    const int u = unit_start(w, c1, c2, n_first);
     int lo = 0, hi = n_tiles - 1;
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
@@ -609,10 +650,11 @@ patch_kernel(int32_t L, int32_t Hkv, int32_t D, int64_t t_total, int32_t n_seqs,
              const uint16_t* __restrict__ vf, uint16_t* __restrict__ kc,
              uint16_t* __restrict__ vc, uint16_t* __restrict__ vh,
              const int32_t* __restrict__ cu_seqlens, int32_t n_tiles, int32_t tile_slots,
-             int32_t rows_per_tile, int32_t n_wg, int32_t n_wg_max, int32_t* __restrict__ plan) {
+             int32_t rows_per_tile, int32_t n_wg, int32_t n_first, int32_t n_wg_max,
+             int32_t* __restrict__ plan) {
   if (plan != nullptr && blockIdx.x == gridDim.x - 1) {
     build_plan(n_tiles, tile_slots, Hkv, t_total, cu_seqlens, n_seqs, rows, cu_rows,
-               rows_per_layer, rows_per_tile, n_wg, n_wg_max, plan);
+               rows_per_layer, rows_per_tile, n_wg, n_first, n_wg_max, plan);
     return;
   }
   const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
@@ -646,44 +688,67 @@ patch_kernel(int32_t L, int32_t Hkv, int32_t D, int64_t t_total, int32_t n_seqs,
 // Two launch shapes:
 //  * whole tiles (many tiles): workgroup t finishes tile t;
 //  * balanced ranges (few tiles): workgroup w walks the tiles that overlap its
-//    units [w C, (w+1) C); tiles covered whole are finished here, the cut ones
-//    (at most its first and its last) leave partial records 2w and 2w + 1.
+//    units [unit_start(w), unit_start(w + 1)); a tile whose blocks it covers
+//    whole is finished here, the cut ones (at most its first and its last)
+//    leave partial records 2w and 2w + 1.
 template <int D>
 __global__ void __launch_bounds__(kThreads, KVB_ATTN_WG_PER_CU)
 attn_kernel(int32_t balanced, int32_t n_tiles, int32_t Hq, int32_t Hkv, int32_t log2g,
             int64_t t_total, const int32_t* __restrict__ cu_seqlens, int32_t n_seqs,
             const int32_t* __restrict__ rows, const int32_t* __restrict__ cu_rows,
             int32_t rows_per_layer, int32_t rows_per_tile, int32_t tile_slots,
-            const int32_t* __restrict__ plan, int32_t n_rec, const uint16_t* __restrict__ q,
-            const uint16_t* __restrict__ kc, const uint16_t* __restrict__ v16, float c_log2,
-            int32_t out_f32, void* __restrict__ out, float* __restrict__ parts) {
+            const int32_t* __restrict__ plan, int32_t n_wg_max, int32_t n_rec,
+            const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
+            const uint16_t* __restrict__ v16, float c_log2, int32_t out_f32,
+            void* __restrict__ out, float* __restrict__ parts) {
   using C = AttnCfg<D>;
   __shared__ __attribute__((aligned(1024))) char k_ring[kStages * C::BLK];
   __shared__ __attribute__((aligned(1024))) char v_ring[kStages * C::BLK];
   if (!balanced) {
     const int t = blockIdx.x;
+    const int lg = t / tile_slots;
+    const int64_t set = rows_per_layer ? lg / Hkv : 0;
+    Tile tile;
+    if (!find_tile(cu_rows + set * (n_seqs + 1), n_seqs, rows_per_tile, t % tile_slots, &tile))
+      return;
+    SegTile tl;
+    tl.lg = lg;
+    tl.r_begin = tile.r_begin;
+    tl.r_end = tile.r_end;
+    tl.kstart = cu_seqlens[tile.b];
+    tl.kend = min(rows[set * t_total + tile.r_end - 1] + 1, (int)t_total);
     const int whole = (int)((t_total + kKB - 1) / kKB) + 1;
-    attend_segment<D>(t / tile_slots, t % tile_slots, 0, whole, -1, n_rec, k_ring, v_ring, Hq,
-                      Hkv, log2g, t_total, cu_seqlens, n_seqs, rows, cu_rows, rows_per_layer,
-                      rows_per_tile, q, kc, v16, c_log2, out_f32, out, parts);
+    attend_segment<D>(tl, 0, whole, -1, n_rec, k_ring, v_ring, Hq, Hkv, log2g, t_total, rows,
+                      rows_per_layer, q, kc, v16, c_log2, out_f32, out, parts);
     return;
   }
   const int w = blockIdx.x;
-  const int chunk = plan[0], total = plan[1];
-  const int32_t* prefix = plan + 2;
-  int u = w * chunk;
-  const int u_end = min(u + chunk, total);
-  int t = plan[3 + n_tiles + w];
+  const int c1 = plan[0], c2 = plan[1], nf = plan[2], total = plan[3];
+  const int32_t* prefix = plan + 4;
+  const int4* meta = reinterpret_cast<const int4*>(plan + tile_meta_offset(n_tiles, n_wg_max));
+  int u = unit_start(w, c1, c2, nf);
+  const int u_end = min(unit_start(w + 1, c1, c2, nf), total);
+  int t = plan[5 + n_tiles + w];
   for (int seg = 0; u < u_end && t < n_tiles; ++t) {
     const int p0 = prefix[t], p1 = prefix[t + 1];
     if (p1 <= u) continue;  // empty tile (or before the range)
     const int e = min(u_end, p1);
-    const int rec = (u == p0 && p1 <= u_end) ? -1 : 2 * w + (seg == 0 ? 0 : 1);
-    attend_segment<D>(t / tile_slots, t % tile_slots, u - p0, e - p0, rec, n_rec, k_ring, v_ring,
-                      Hq, Hkv, log2g, t_total, cu_seqlens, n_seqs, rows, cu_rows, rows_per_layer,
-                      rows_per_tile, q, kc, v16, c_log2, out_f32, out, parts);
+    // units [p0, p0 + kSegCost) of a tile stand for its fixed cost and hold no block
+    const int b_lo = max(u - p0 - kSegCost, 0), b_hi = max(e - p0 - kSegCost, 0);
+    if (b_hi > b_lo) {
+      const int rec = (u <= p0 + kSegCost && p1 <= u_end) ? -1 : 2 * w + (seg == 0 ? 0 : 1);
+      const int4 mt = meta[t];
+      SegTile tl;
+      tl.lg = t / tile_slots;
+      tl.r_begin = mt.x;
+      tl.r_end = mt.y;
+      tl.kstart = mt.z;
+      tl.kend = mt.w;
+      attend_segment<D>(tl, b_lo, b_hi, rec, n_rec, k_ring, v_ring, Hq, Hkv, log2g, t_total, rows,
+                        rows_per_layer, q, kc, v16, c_log2, out_f32, out, parts);
+      ++seg;
+    }
     u = e;
-    ++seg;
   }
 }
 
@@ -698,11 +763,12 @@ combine_kernel(int32_t n_tiles, int32_t n_wg_max, int32_t Hq, int32_t Hkv, int32
                int32_t tile_slots, const int32_t* __restrict__ plan, int32_t n_rec,
                int32_t out_f32, void* __restrict__ out, const float* __restrict__ parts) {
   const int t = blockIdx.x;
-  const int chunk = plan[0];
-  const int p0 = plan[2 + t], p1 = plan[3 + t];
+  const int c1 = plan[0], c2 = plan[1], nf = plan[2];
+  const int p0 = plan[4 + t], p1 = plan[5 + t];
   const int4 mt = reinterpret_cast<const int4*>(plan + tile_meta_offset(n_tiles, n_wg_max))[t];
   if (p1 <= p0) return;
-  const int w_a = p0 / chunk, w_b = (p1 - 1) / chunk;
+  // the tile's blocks are units [p0 + kSegCost, p1)
+  const int w_a = unit_owner(p0 + kSegCost, c1, c2, nf), w_b = unit_owner(p1 - 1, c1, c2, nf);
   if (w_a == w_b) return;  // finished by one workgroup
   constexpr int Q8 = D / 8;  // 8-channel pieces per query vector
   const int e = blockIdx.y * blockDim.x + threadIdx.x;
@@ -716,8 +782,9 @@ combine_kernel(int32_t n_tiles, int32_t n_wg_max, int32_t Hq, int32_t Hkv, int32
   const int64_t set = rows_per_layer ? l : 0;
   const int tq = rows[set * t_total + row_idx];
   // the tile is the first segment of every workgroup after w_a, and of w_a
-  // only if w_a's range starts exactly at the tile
-  const int rec_a = 2 * w_a + (w_a * chunk < p0 ? 1 : 0);
+  // only if w_a's range starts inside the tile (a range that starts before it
+  // ends with blocks of an earlier tile)
+  const int rec_a = 2 * w_a + (unit_start(w_a, c1, c2, nf) < p0 ? 1 : 0);
   const int n_parts = w_b - w_a + 1;
   const uint16_t* o16 = reinterpret_cast<const uint16_t*>(parts);
   const float* ml = reinterpret_cast<const float*>(reinterpret_cast<const char*>(parts) +
@@ -806,8 +873,8 @@ bool attn_plan(int n_layers, int n_q_heads, int n_kv_heads, int head_dim, int64_
   const int64_t full_tiles = ((int64_t)max_rows + rows_per_tile - 1) / rows_per_tile;
   const int64_t tile_slots = full_tiles + n_seqs;
   const int64_t n_tiles = (int64_t)n_layers * n_kv_heads * tile_slots;
-  // block units must fit int32: at most n_tiles * ceil(max_seq_len / 32)
-  if (n_tiles * ((max_seq_len + kKB - 1) / kKB) > INT32_MAX / 2) return false;
+  // work units must fit int32: at most n_tiles * (ceil(max_seq_len / 32) + kSegCost)
+  if (n_tiles * ((max_seq_len + kKB - 1) / kKB + kSegCost) > INT32_MAX / 2) return false;
   plan->rows_per_tile = rows_per_tile;
   plan->tile_slots = (int)tile_slots;
   plan->n_tiles = (int)n_tiles;
@@ -843,6 +910,8 @@ hipError_t launch_sparse_attn(const AttnPlan& plan, int n_layers, int n_q_heads,
   float* parts = reinterpret_cast<float*>(wsb + plan.parts_offset);
   int n_wg = resident_workgroups();
   if (n_wg > plan.n_wg_max) n_wg = plan.n_wg_max;
+  // first-slot workgroups (see kFirstShareNum) exist only with two per CU
+  const int n_first = (KVB_ATTN_WG_PER_CU == 2 && n_wg == resident_workgroups()) ? n_wg / 2 : 0;
   // enough tiles to keep every resident workgroup busy twice over: one tile per
   // workgroup, no partials; otherwise balanced ranges
   const int balanced = plan.n_tiles < 2 * n_wg;
@@ -854,7 +923,7 @@ hipError_t launch_sparse_attn(const AttnPlan& plan, int n_layers, int n_q_heads,
                          n_kv_heads, head_dim, t_total, n_seqs, rows, cu_rows, rows_per_layer,
                          max_rows, k_fresh, v_fresh, k_cache, v_cache,
                          plan.v16_in_ws ? nullptr : v_cache_f16, cu_seqlens, plan.n_tiles,
-                         plan.tile_slots, plan.rows_per_tile, n_wg, plan.n_wg_max,
+                         plan.tile_slots, plan.rows_per_tile, n_wg, n_first, plan.n_wg_max,
                          balanced ? wplan : nullptr);
   }
   if (plan.v16_in_ws) {
@@ -870,8 +939,8 @@ hipError_t launch_sparse_attn(const AttnPlan& plan, int n_layers, int n_q_heads,
 #define KVB_ATTN(D)                                                                              \
   hipLaunchKernelGGL(attn_kernel<D>, grid, dim3(kThreads), 0, s, balanced, plan.n_tiles, n_q_heads,\
                      n_kv_heads, log2g, t_total, cu_seqlens, n_seqs, rows, cu_rows,              \
-                     rows_per_layer, plan.rows_per_tile, plan.tile_slots, wplan, plan.n_rec, q,   \
-                     k_cache, v16, c_log2, out_f32, out, parts)
+                     rows_per_layer, plan.rows_per_tile, plan.tile_slots, wplan, plan.n_wg_max,   \
+                     plan.n_rec, q, k_cache, v16, c_log2, out_f32, out, parts)
 #define KVB_COMBINE(D)                                                                           \
   hipLaunchKernelGGL(combine_kernel<D>, dim3(plan.n_tiles, kQT * (D / 8) / 256), dim3(256), 0, s, \
                      plan.n_tiles, plan.n_wg_max, n_q_heads, n_kv_heads, log2g, t_total, rows,    \
