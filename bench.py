@@ -176,6 +176,33 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    ref = [t.clone() for t in (pb.k_cache, pb.v_cache, pb.delta, pb.rows, pb.cu_rows, pb.out)]
+
+    # Headline: the whole step (stitch, deviation + selection, the attention
+    # calls) captured once in a HIP graph and replayed, so the per-layer
+    # launches run back to back as a model's captured forward would run them
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    g0, g1 = ev(), ev()
+    g0.record(stream)
+    for _ in range(args.steps):
+        graph.replay()
+    g1.record(stream)
+    torch.cuda.synchronize()
+    ms_step_graph = g0.elapsed_time(g1) / args.steps
+    graph_same = all(torch.equal(a, b) for a, b in
+                     zip(ref, (pb.k_cache, pb.v_cache, pb.delta, pb.rows, pb.cu_rows, pb.out)))
+    if not graph_same:
+        log("[bench] graph replay differs from the eager step: reporting the eager time")
+    del graph
+
+    # Eager steps with HIP events around every call: per-kernel times and the
+    # attention call's duration for the roofline
     n_ev = 3 + (1 if args.attn_all_layers else L)
     recs = [[ev() for _ in range(n_ev)] for _ in range(args.steps)]
     start, stop = ev(), ev()
@@ -186,11 +213,13 @@ def main():
     stop.record(stream)
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(stop)
-    ms_step = total_ms / args.steps
+    ms_step_eager = total_ms / args.steps
+    ms_step = ms_step_graph if graph_same else ms_step_eager
     st_ms = np.mean([r[0].elapsed_time(r[1]) for r in recs])
     dv_ms = np.mean([r[1].elapsed_time(r[2]) for r in recs])
     at_ms = np.array([[r[2 + j].elapsed_time(r[3 + j]) for j in range(n_ev - 3)] for r in recs])
     attn_ms_launch = float(at_ms.mean())
+    attn_p10, attn_p50, attn_p90 = (float(np.percentile(at_ms, p)) for p in (10, 50, 90))
 
     rows = pb.rows.cpu().numpy()
     cu = pb.cu_rows.cpu().numpy()
@@ -203,7 +232,7 @@ def main():
     # timed call neither hits its inputs in the cache nor pays for another
     # kernel's write-back
     flush = torch.ones(args.flush_mb << 18, dtype=torch.float32, device="cuda")
-    st_f, dv_f = [], []
+    st_f, dv_f, d_f = [], [], []
     for _ in range(5):
         flush.sum()
         torch.cuda.synchronize()
@@ -219,11 +248,20 @@ def main():
         pipeline.deviation_topk(di, pb)
         c.record(stream)
         torch.cuda.synchronize()
+        flush.sum()
+        torch.cuda.synchronize()
+        d0, d1 = ev(), ev()
+        d0.record(stream)
+        pipeline.deviation(di, pb)
+        d1.record(stream)
+        torch.cuda.synchronize()
         st_f.append(a.elapsed_time(b))
         dv_f.append(b2.elapsed_time(c))
+        d_f.append(d0.elapsed_time(d1))
     del flush
     st_gbs = st_bytes / (np.median(st_f) * 1e-3) / 1e9
     dv_gbs = dev_bytes / (np.median(dv_f) * 1e-3) / 1e9
+    d_gbs = dev_bytes / (np.median(d_f) * 1e-3) / 1e9
 
     if args.calibrate_copy_mb:
         src = torch.ones(args.calibrate_copy_mb << 20, dtype=torch.uint8, device="cuda")
@@ -254,6 +292,7 @@ def main():
             "kivi_bits": w.bits, "k_group": w.k_group, "v_group": w.v_group,
             "cached_chunks": s.n_pool, "recompute": f"{w.rho_num}/{w.rho_den} per layer",
             "attention_launches": "one per layer" if not args.attn_all_layers else "one for all layers",
+            "step_timing": "HIP graph replay" if graph_same else "eager (graph replay differed)",
             "parallelism": "single GPU",
         },
         "roofline": {
@@ -262,13 +301,18 @@ def main():
             "unit": "TFLOP/s", "frac": attn_tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": traffic,
             "traffic_note": traffic_note,
             "flops_per_launch": attn_flops_launch, "ms_per_launch": attn_ms_launch,
+            "ms_per_launch_p10_p50_p90": [attn_p10, attn_p50, attn_p90],
+            "timing": "HIP events around each call in eager steps",
         },
         "kernels": {
+            "ms_per_step_eager": ms_step_eager, "ms_per_step_graph": ms_step_graph,
             "stitch_ms": float(st_ms), "deviation_topk_ms": float(dv_ms),
             "sparse_attn_ms_per_step": float(at_ms.sum(axis=1).mean()),
             "stitch_GBps_flushed": st_gbs, "stitch_hbm_frac": st_gbs / HBM_PEAK_GBS,
             "stitch_bytes": st_bytes,
-            "deviation_topk_GBps_flushed": dv_gbs, "deviation_hbm_frac": dv_gbs / HBM_PEAK_GBS,
+            "deviation_GBps_flushed": d_gbs, "deviation_hbm_frac": d_gbs / HBM_PEAK_GBS,
+            "deviation_topk_GBps_flushed": dv_gbs, "deviation_topk_hbm_frac": dv_gbs / HBM_PEAK_GBS,
+            "select_ms_flushed": float(np.median(dv_f) - np.median(d_f)),
             "deviation_bytes": dev_bytes,
             "selected_rows_per_layer": float(np.mean(cu[:, -1])),
         },

@@ -47,6 +47,8 @@
 // operands, so its order inside the MFMA does not matter.
 #include <math.h>
 
+#include <type_traits>
+
 #include "kvb_device.h"
 #include "kvb_internal.h"
 
@@ -425,14 +427,13 @@ __device__ __forceinline__ void attend_segment(
   const LoadOffsets<D> lo = load_offsets<D>(wave, lane);
   const int nblk = (k_hi - k_lo + kKB - 1) / kKB;
   static_assert(kStages == 4, "stage index arithmetic assumes a 4-deep ring");
-  auto kst = [&](int b) { return k_ring + (b & 3) * C::BLK; };  // ring stage of block b
-  auto vst = [&](int b) { return v_ring + (b & 3) * C::BLK; };
 
   // The first three blocks depend only on the tile: they are requested while
   // the query rows are on their way.
-  issue_block<D>(krs, vrs, k_lo, lo, kst(0), vst(0), wave);
-  if (nblk > 1) issue_block<D>(krs, vrs, k_lo + kKB, lo, kst(1), vst(1), wave);
-  if (nblk > 2) issue_block<D>(krs, vrs, k_lo + 2 * kKB, lo, kst(2), vst(2), wave);
+  issue_block<D>(krs, vrs, k_lo, lo, k_ring, v_ring, wave);
+  if (nblk > 1) issue_block<D>(krs, vrs, k_lo + kKB, lo, k_ring + C::BLK, v_ring + C::BLK, wave);
+  if (nblk > 2)
+    issue_block<D>(krs, vrs, k_lo + 2 * kKB, lo, k_ring + 2 * C::BLK, v_ring + 2 * C::BLK, wave);
 
   const bool qvalid = t_q >= tl.kstart && t_q < tl.kend;  // rows outside the prompt are skipped
   if (!qvalid) t_q = -1;
@@ -459,15 +460,17 @@ __device__ __forceinline__ void attend_segment(
   st.m_raw = -INFINITY;
   st.l_part = 0.0f;
 
-  // Software pipeline over blocks: iteration j computes the scores of block
-  // j + 1 on the matrix cores while the vector units turn the scores of block j
-  // into probabilities, then accumulates P V for block j.  The ring holds
-  // blocks j .. j + 3; block j + 3 is requested once every wave has finished
-  // block j - 1 (the barrier), whose stage it reuses.
+  // Software pipeline over blocks: step j computes the scores of block j + 1 on
+  // the matrix cores while the vector units turn the scores of block j into
+  // probabilities, then accumulates P V for block j.  The ring holds blocks
+  // j .. j + 3; block j + 3 is requested once every wave has finished block
+  // j - 1 (the barrier), whose stage it reuses.  The loop is unrolled over the
+  // four ring stages so every LDS address is a per-lane base plus a constant.
   bf16x8 kr[C::NS];
-  read_k<D>(kst(0), lane, kr);
+  read_k<D>(k_ring, lane, kr);
   f32x16 sacc = scores<D>(kr, qop);
-  for (int j = 0; j < nblk; ++j) {
+  auto step = [&](auto stage, int j) {
+    constexpr int S = decltype(stage)::value;  // ring stage of block j
     const int kb = k_lo + j * kKB;
     if (j + 2 < nblk)
       wait_vmcnt<2 * C::LOADS>();  // block j + 1 landed, block j + 2 may be in flight
@@ -475,11 +478,13 @@ __device__ __forceinline__ void attend_segment(
       wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
-    if (j + 3 < nblk) issue_block<D>(krs, vrs, kb + 3 * kKB, lo, kst(j + 3), vst(j + 3), wave);
-    // on the last iteration this reads a stale stage; those scores are never used
-    read_k<D>(kst(j + 1), lane, kr);
+    if (j + 3 < nblk)
+      issue_block<D>(krs, vrs, kb + 3 * kKB, lo, k_ring + ((S + 3) & 3) * C::BLK,
+                     v_ring + ((S + 3) & 3) * C::BLK, wave);
+    // on the last step this reads a stale stage; those scores are never used
+    read_k<D>(k_ring + ((S + 1) & 3) * C::BLK, lane, kr);
     f16x8 vr[2][C::ND];
-    read_v<D>(vst(j), lane, vr);
+    read_v<D>(v_ring + S * C::BLK, lane, vr);
     const bool full = (kb + kKB - 1 <= t_min) && (kb + kKB <= k_hi);
     f16x8 pb[2];
     softmax_block<D>(sacc, st, c_log2, full, kb, t_q, k_hi, lane, pb);
@@ -489,7 +494,21 @@ __device__ __forceinline__ void attend_segment(
 #pragma unroll
       for (int dt = 0; dt < C::ND; ++dt)
         st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[ks][dt], pb[ks], st.o[dt], 0, 0, 0);
+  };
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  using S2 = std::integral_constant<int, 2>;
+  using S3 = std::integral_constant<int, 3>;
+  int j = 0;
+  for (; j + 4 <= nblk; j += 4) {
+    step(S0{}, j);
+    step(S1{}, j + 1);
+    step(S2{}, j + 2);
+    step(S3{}, j + 3);
   }
+  if (j < nblk) step(S0{}, j);
+  if (j + 1 < nblk) step(S1{}, j + 1);
+  if (j + 2 < nblk) step(S2{}, j + 2);
 
   if (!qvalid) return;
   const float l_run = sum_halves(st.l_part);

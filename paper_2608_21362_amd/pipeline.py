@@ -196,6 +196,13 @@ def stitch(di: DeviceInputs, pb: PathBuffers, out_dtype=kvb.KVB_BF16, k_out=None
                    stream)
 
 
+def deviation(di: DeviceInputs, pb: PathBuffers, stream=None):
+    """Deviation of the stitched K against the fresh K only (no selection)."""
+    w = di.w
+    kvb.kvb_deviation(di.n_layers, w.n_kv_heads, w.head_dim, w.t_total, pb.k_cache, di.k_fresh,
+                      None, None, w.per_layer, pb.delta, stream)
+
+
 def deviation_topk(di: DeviceInputs, pb: PathBuffers, stream=None):
     w = di.w
     kvb.kvb_deviation_topk(di.n_layers, w.n_kv_heads, w.head_dim, w.t_total, di.cu_seqlens,
