@@ -646,16 +646,20 @@ __device__ __forceinline__ void build_plan(
     prefix[n_tiles] = total;
   }
   __syncthreads();
-  // tile holding unit unit_start(w): the largest t with prefix[t] <= unit_start(w)
-  for (int w = tid; w < n_wg; w += nt) {
-    const int u = unit_start(w, c1, c2, n_first);
-    int lo = 0, hi = n_tiles - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (prefix[mid] <= u) lo = mid; else hi = mid - 1;
+  // tile holding unit unit_start(w): every non-empty tile [p0, p1) writes the
+  // workgroups whose first unit lies in it (one pass, no search); workgroups
+  // that start past the last unit get n_tiles (they have no work)
+  for (int t = tid; t < n_tiles; t += nt) {
+    const int p0 = prefix[t], p1 = prefix[t + 1];
+    if (p1 <= p0) continue;
+    for (int w = unit_owner(p0, c1, c2, n_first); w < n_wg; ++w) {
+      const int u = unit_start(w, c1, c2, n_first);
+      if (u >= p1) break;
+      if (u >= p0) first[w] = t;
     }
-    first[w] = lo;
   }
+  for (int w = tid; w < n_wg; w += nt)
+    if (unit_start(w, c1, c2, n_first) >= total) first[w] = n_tiles;
 }
 
 // Patch: cache[l][h][t] <- fresh[l][h][t] for every selected row t (both

@@ -7,8 +7,8 @@
 //
 // Key jobs: one thread takes 4 consecutive tokens (one statistic group,
 // Gk % 4 == 0) and 8 channel pairs (j, j + d/2); statistics and the chunk's
-// rotation row are loaded and widened to double once per job.  Value pieces:
-// one thread takes one token and 8 consecutive channels (one statistic group,
+// rotation row are loaded once per job and widened to double at each use.
+// Value pieces: one thread takes one token and 8 consecutive channels (one statistic group,
 // Gv % 8 == 0; the API asks Gv % 16), so 16 (d = 128) or 8 (d = 64) lanes
 // store a whole row and a wave's stores are contiguous.  Every value input of
 // the thread is loaded before the key work starts, so those loads overlap it.
@@ -83,7 +83,8 @@ stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
       const int g = u0 / Gk;
       const float* sc = k_scale + (slab * ngk + g) * D;
       const float* zr = k_zero + (slab * ngk + g) * D;
-      double s_lo[8], s_hi[8], z_lo[8], z_hi[8], cs[8], sn[8];
+      // kept as float (half the registers of double) and widened exactly at use
+      float s_lo[8], s_hi[8], z_lo[8], z_hi[8], cs[8], sn[8];
 #pragma unroll
       for (int k = 0; k < 8; k += 4) {
         const float4 a = *reinterpret_cast<const float4*>(sc + j0 + k);
@@ -116,12 +117,12 @@ stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
         float ylo[8], yhi[8];
 #pragma unroll
         for (int k = 0; k < 8; ++k) {
-          const double xl = __builtin_fma((double)code_at<BITS>(wl, k), s_lo[k], z_lo[k]);
-          const double xh = __builtin_fma((double)code_at<BITS>(wh, k), s_hi[k], z_hi[k]);
-          const double a = xl * cs[k];
-          const double b = xh * sn[k];
-          const double e = xh * cs[k];
-          const double f = xl * sn[k];
+          const double xl = __builtin_fma((double)code_at<BITS>(wl, k), (double)s_lo[k], (double)z_lo[k]);
+          const double xh = __builtin_fma((double)code_at<BITS>(wh, k), (double)s_hi[k], (double)z_hi[k]);
+          const double a = xl * (double)cs[k];
+          const double b = xh * (double)sn[k];
+          const double e = xh * (double)cs[k];
+          const double f = xl * (double)sn[k];
           ylo[k] = (float)(a - b);
           yhi[k] = (float)(e + f);
         }
