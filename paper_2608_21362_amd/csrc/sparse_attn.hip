@@ -19,7 +19,7 @@
 // fill the MFMA N dimension, each of the 4 waves owning 32 query vectors
 // (32/G rows x G heads).  A workgroup runs one whole tile, or a range of key
 // blocks that may span tiles (see attn_kernel).  Keys stream in blocks of 32
-// through a four-stage LDS ring filled by asynchronous global->LDS loads (no
+// through a five-stage LDS ring filled by asynchronous global->LDS loads (no
 // VGPR staging), XOR-swizzled on 16-byte chunks so the operand reads below are
 // free of bank conflicts:
 //
@@ -38,7 +38,8 @@
 //                                           from the S^T accumulators
 //
 // The loop is software-pipelined: the scores of block j+1 are computed while
-// block j's probabilities are formed, with one barrier per block.
+// block j's probabilities are formed, and the LDS operands of the next step
+// are read at the end of the current one; one barrier per block.
 //
 // The accumulator layout of a 32x32 MFMA gives lane half h the keys
 // {4h..4h+3, 8+4h..8+4h+3} of every 16-key step; the transpose reads fetch V
@@ -76,7 +77,7 @@ constexpr int kQT = kQW * kWaves;       // query vectors per workgroup
 #define KVB_ATTN_WG_PER_CU 2
 #endif
 constexpr int kKB = 32;                 // keys per block = one 32-row MFMA tile
-constexpr int kStages = 4;              // LDS ring depth (blocks in flight: 2 ahead)
+constexpr int kStages = 5;              // LDS ring depth (80 KiB per workgroup at d = 128)
 constexpr int kAttnMaxWorkgroups = 1024;  // attention workgroups (sizes the partial records)
 // Balanced ranges charge every tile a fixed cost, in 32-key block units, for a
 // segment's start (tile rows, queries and the first blocks fetched) and end
@@ -226,7 +227,7 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)LDS_PTR(const char, p);
 }
 
-// Issue the asynchronous loads of one 64-key block of K (bf16) and V (fp16)
+// Issue the asynchronous loads of one 32-key block of K (bf16) and V (fp16)
 // into one LDS stage.  The buffer resources cover exactly the cache rows of
 // this (layer, kv head); rows past the end read as zero (their scores are
 // masked).
@@ -426,14 +427,16 @@ __device__ __forceinline__ void attend_segment(
   const i32x4 vrs = buffer_rsrc(v16 + kv_base, T * C::ROWB);
   const LoadOffsets<D> lo = load_offsets<D>(wave, lane);
   const int nblk = (k_hi - k_lo + kKB - 1) / kKB;
-  static_assert(kStages == 4, "stage index arithmetic assumes a 4-deep ring");
+  static_assert(kStages == 5, "stage index arithmetic assumes a 5-deep ring");
 
-  // The first three blocks depend only on the tile: they are requested while
+  // The first four blocks depend only on the tile: they are requested while
   // the query rows are on their way.
   issue_block<D>(krs, vrs, k_lo, lo, k_ring, v_ring, wave);
   if (nblk > 1) issue_block<D>(krs, vrs, k_lo + kKB, lo, k_ring + C::BLK, v_ring + C::BLK, wave);
   if (nblk > 2)
     issue_block<D>(krs, vrs, k_lo + 2 * kKB, lo, k_ring + 2 * C::BLK, v_ring + 2 * C::BLK, wave);
+  if (nblk > 3)
+    issue_block<D>(krs, vrs, k_lo + 3 * kKB, lo, k_ring + 3 * C::BLK, v_ring + 3 * C::BLK, wave);
 
   const bool qvalid = t_q >= tl.kstart && t_q < tl.kend;  // rows outside the prompt are skipped
   if (!qvalid) t_q = -1;
@@ -460,55 +463,69 @@ __device__ __forceinline__ void attend_segment(
   st.m_raw = -INFINITY;
   st.l_part = 0.0f;
 
-  // Software pipeline over blocks: step j computes the scores of block j + 1 on
-  // the matrix cores while the vector units turn the scores of block j into
-  // probabilities, then accumulates P V for block j.  The ring holds blocks
-  // j .. j + 3; block j + 3 is requested once every wave has finished block
-  // j - 1 (the barrier), whose stage it reuses.  The loop is unrolled over the
-  // four ring stages so every LDS address is a per-lane base plus a constant.
+  // Software pipeline over blocks: step j turns the scores of block j into
+  // probabilities on the vector units while the matrix cores compute the
+  // scores of block j + 1, then accumulates P V for block j, and last reads
+  // the LDS operands of the next step (K of block j + 2, V of block j + 1), so
+  // no step starts by waiting on LDS.  The ring holds blocks j .. j + 4: a step
+  // waits for block j + 2 to land (block j + 3 may be in flight) and, after
+  // the barrier that every wave reaches once done with block j - 1, requests
+  // block j + 4 into that block's stage.  The waves raise their issue priority
+  // while they send P V to the matrix cores.  The loop is unrolled over the
+  // five ring stages so every LDS address is a per-lane base plus a constant.
   bf16x8 kr[C::NS];
   read_k<D>(k_ring, lane, kr);
   f32x16 sacc = scores<D>(kr, qop);
+  f16x8 vr[2][C::ND];
+  read_k<D>(k_ring + C::BLK, lane, kr);  // stale when nblk == 1: never used
+  read_v<D>(v_ring, lane, vr);
   auto step = [&](auto stage, int j) {
     constexpr int S = decltype(stage)::value;  // ring stage of block j
     const int kb = k_lo + j * kKB;
-    if (j + 2 < nblk)
-      wait_vmcnt<2 * C::LOADS>();  // block j + 1 landed, block j + 2 may be in flight
+    if (j + 3 < nblk)
+      wait_vmcnt<2 * C::LOADS>();  // block j + 2 landed, block j + 3 may be in flight
     else
       wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
-    if (j + 3 < nblk)
-      issue_block<D>(krs, vrs, kb + 3 * kKB, lo, k_ring + ((S + 3) & 3) * C::BLK,
-                     v_ring + ((S + 3) & 3) * C::BLK, wave);
-    // on the last step this reads a stale stage; those scores are never used
-    read_k<D>(k_ring + ((S + 1) & 3) * C::BLK, lane, kr);
-    f16x8 vr[2][C::ND];
-    read_v<D>(v_ring + S * C::BLK, lane, vr);
+    if (j + 4 < nblk)
+      issue_block<D>(krs, vrs, kb + 4 * kKB, lo, k_ring + ((S + 4) % 5) * C::BLK,
+                     v_ring + ((S + 4) % 5) * C::BLK, wave);
     const bool full = (kb + kKB - 1 <= t_min) && (kb + kKB <= k_hi);
     f16x8 pb[2];
     softmax_block<D>(sacc, st, c_log2, full, kb, t_q, k_hi, lane, pb);
     sacc = scores<D>(kr, qop);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
       for (int dt = 0; dt < C::ND; ++dt)
         st.o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[ks][dt], pb[ks], st.o[dt], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_setprio(0);
+    // operands of the next step (landed and visible since this step's
+    // barrier; stale past the end of the segment, never used)
+    read_k<D>(k_ring + ((S + 2) % 5) * C::BLK, lane, kr);
+    read_v<D>(v_ring + ((S + 1) % 5) * C::BLK, lane, vr);
   };
   using S0 = std::integral_constant<int, 0>;
   using S1 = std::integral_constant<int, 1>;
   using S2 = std::integral_constant<int, 2>;
   using S3 = std::integral_constant<int, 3>;
+  using S4 = std::integral_constant<int, 4>;
   int j = 0;
-  for (; j + 4 <= nblk; j += 4) {
+  for (; j + 5 <= nblk; j += 5) {
     step(S0{}, j);
     step(S1{}, j + 1);
     step(S2{}, j + 2);
     step(S3{}, j + 3);
+    step(S4{}, j + 4);
   }
   if (j < nblk) step(S0{}, j);
   if (j + 1 < nblk) step(S1{}, j + 1);
   if (j + 2 < nblk) step(S2{}, j + 2);
+  if (j + 3 < nblk) step(S3{}, j + 3);
 
   if (!qvalid) return;
   const float l_run = sum_halves(st.l_part);
