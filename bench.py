@@ -44,8 +44,10 @@ def algorithmic(w, s, rows_per_set, cu_rows_per_set):
 
     Stitch: the codes and statistics it reads, the bf16 K and V rows it writes
     and the fp16 shadow of V it keeps for the attention.  Deviation: the cache
-    and fresh K rows it reads (bf16) and the deviation it writes.  Attention:
-    4 d Hq flops per (selected query row, visible key): QK^T and PV."""
+    and fresh K rows it reads (bf16) and the deviation it writes.  Fused stitch +
+    deviation: the stitch's bytes plus the fresh K rows of the stitched chunks
+    and their deviations.  Attention: 4 d Hq flops per (selected query row,
+    visible key): QK^T and PV."""
     L, H, d, C, T, Hq = w.n_layers, w.n_kv_heads, w.head_dim, w.chunk_len, w.t_total, w.n_q_heads
     P = s.n_pool
     cb = d * w.bits // 8
@@ -55,13 +57,14 @@ def algorithmic(w, s, rows_per_set, cu_rows_per_set):
     stitch_bytes = codes + stats + stitch_out
     n_sets = rows_per_set.shape[0]
     dev_bytes = 2 * L * H * T * d * 2 + n_sets * T * 4
+    fused_bytes = stitch_bytes + P * L * H * C * d * 2 + L * P * C * 4
     pos = s.positions().astype(np.int64)
     flops_per_layer = []
     for l in range(L):
         si = l if w.per_layer else 0
         r = rows_per_set[si, : cu_rows_per_set[si, -1]]
         flops_per_layer.append(4.0 * d * Hq * float(np.sum(pos[r] + 1)))
-    return stitch_bytes, dev_bytes, np.array(flops_per_layer)
+    return stitch_bytes, dev_bytes, fused_bytes, np.array(flops_per_layer)
 
 
 def committed_traffic(workload):
@@ -121,6 +124,9 @@ def main():
     ap.add_argument("--workload", default="qwen_36l_8k")
     ap.add_argument("--attn-all-layers", action="store_true",
                     help="one attention launch for all layers (ceiling variant)")
+    ap.add_argument("--unfused", action="store_true",
+                    help="separate stitch and deviation + selection calls instead of the fused "
+                         "stitch + deviation call followed by selection")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=24,
                     help="layers of the oracle timed for cpu_baseline (scaled to the whole step)")
@@ -154,13 +160,21 @@ def main():
     ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     L = di.n_layers
 
+    fused = not args.unfused
+
     def step(rec=None):
         if rec is not None:
             rec[0].record(stream)
-        pipeline.stitch(di, pb)
+        if fused:
+            pipeline.stitch_deviation(di, pb)
+        else:
+            pipeline.stitch(di, pb)
         if rec is not None:
             rec[1].record(stream)
-        pipeline.deviation_topk(di, pb)
+        if fused:
+            pipeline.select(di, pb)
+        else:
+            pipeline.deviation_topk(di, pb)
         if rec is not None:
             rec[2].record(stream)
         if args.attn_all_layers:
@@ -223,7 +237,7 @@ def main():
 
     rows = pb.rows.cpu().numpy()
     cu = pb.cu_rows.cpu().numpy()
-    st_bytes, dev_bytes, flops = algorithmic(w, s, rows, cu)
+    st_bytes, dev_bytes, sd_bytes, flops = algorithmic(w, s, rows, cu)
     attn_flops_launch = float(flops.mean()) if not args.attn_all_layers else float(flops.sum())
     attn_tflops = attn_flops_launch / (attn_ms_launch * 1e-3) / 1e12
 
@@ -232,14 +246,15 @@ def main():
     # timed call neither hits its inputs in the cache nor pays for another
     # kernel's write-back
     flush = torch.ones(args.flush_mb << 18, dtype=torch.float32, device="cuda")
-    st_f, dv_f, d_f = [], [], []
+    st_f, dv_f, d_f, sd_f = [], [], [], []
     for _ in range(5):
         # flush, then the timed call right behind it on the same stream (no
         # host synchronisation in between, so the interval holds no idle
         # launch latency)
         for fn, acc in ((lambda: pipeline.stitch(di, pb), st_f),
                         (lambda: pipeline.deviation_topk(di, pb), dv_f),
-                        (lambda: pipeline.deviation(di, pb), d_f)):
+                        (lambda: pipeline.deviation(di, pb), d_f),
+                        (lambda: pipeline.stitch_deviation(di, pb), sd_f)):
             flush.sum()
             a, b = ev(), ev()
             a.record(stream)
@@ -251,6 +266,7 @@ def main():
     st_gbs = st_bytes / (np.median(st_f) * 1e-3) / 1e9
     dv_gbs = dev_bytes / (np.median(dv_f) * 1e-3) / 1e9
     d_gbs = dev_bytes / (np.median(d_f) * 1e-3) / 1e9
+    sd_gbs = sd_bytes / (np.median(sd_f) * 1e-3) / 1e9
 
     if args.calibrate_copy_mb:
         src = torch.ones(args.calibrate_copy_mb << 20, dtype=torch.uint8, device="cuda")
@@ -281,6 +297,8 @@ def main():
             "kivi_bits": w.bits, "k_group": w.k_group, "v_group": w.v_group,
             "cached_chunks": s.n_pool, "recompute": f"{w.rho_num}/{w.rho_den} per layer",
             "attention_launches": "one per layer" if not args.attn_all_layers else "one for all layers",
+            "stitch_and_deviation": "fused (kvb_stitch_deviation, then kvb_select)" if fused
+            else "separate (kvb_stitch, then kvb_deviation_topk)",
             "step_timing": "HIP graph replay" if graph_same else "eager (graph replay differed)",
             "parallelism": "single GPU",
         },
@@ -295,13 +313,16 @@ def main():
         },
         "kernels": {
             "ms_per_step_eager": ms_step_eager, "ms_per_step_graph": ms_step_graph,
-            "stitch_ms": float(st_ms), "deviation_topk_ms": float(dv_ms),
+            ("stitch_deviation_ms" if fused else "stitch_ms"): float(st_ms),
+            ("select_ms" if fused else "deviation_topk_ms"): float(dv_ms),
             "sparse_attn_ms_per_step": float(at_ms.sum(axis=1).mean()),
             "stitch_GBps_flushed": st_gbs, "stitch_hbm_frac": st_gbs / HBM_PEAK_GBS,
             "stitch_bytes": st_bytes,
             "deviation_GBps_flushed": d_gbs, "deviation_hbm_frac": d_gbs / HBM_PEAK_GBS,
             "deviation_topk_GBps_flushed": dv_gbs, "deviation_topk_hbm_frac": dv_gbs / HBM_PEAK_GBS,
             "select_ms_flushed": float(np.median(dv_f) - np.median(d_f)),
+            "stitch_deviation_GBps_flushed": sd_gbs, "stitch_deviation_hbm_frac": sd_gbs / HBM_PEAK_GBS,
+            "stitch_deviation_bytes": sd_bytes,
             "deviation_bytes": dev_bytes,
             "selected_rows_per_layer": float(np.mean(cu[:, -1])),
         },

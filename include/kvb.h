@@ -7,6 +7,8 @@
  *
  *   kvb_stitch          dequantise cached chunks, re-rotate keys to their new
  *                       position (Sec. 4.3, Sec. 3.2 Eq. 3, Sec. 4.5 Eq. 7)
+ *   kvb_stitch_deviation  kvb_stitch plus the deviation of the stitched rows in
+ *                       the same pass (Alg. 2 steps 1-2 fused)
  *   kvb_deviation       per-token cosine deviation (Alg. 2 step 2)
  *   kvb_select          top floor(rho n) rows + seam windows + live rows
  *                       (Alg. 2 step 3, Alg. 1, Sec. 4.1 sinks)
@@ -83,8 +85,9 @@ typedef struct {
   int32_t pool_idx, src_pos, dst_row, dst_pos;
 } kvb_chunk;
 
-/* 2 for this header (version 2 added the optional fp16 shadow of V to
- * kvb_stitch, kvb_sparse_attn and kvb_sparse_attn_workspace_bytes). */
+/* 3 for this header (version 2 added the optional fp16 shadow of V to
+ * kvb_stitch, kvb_sparse_attn and kvb_sparse_attn_workspace_bytes; version 3
+ * added kvb_stitch_deviation). */
 int kvb_abi_version(void);
 
 /* Thread-local message of the last failing call on this thread. */
@@ -178,6 +181,29 @@ kvb_status kvb_stitch(const kvb_pool_layout* pool, int32_t n_pool,
                       const float* rope_cos, const float* rope_sin,
                       int64_t t_total, kvb_dtype out_dtype, void* k_cache, void* v_cache,
                       uint16_t* v_cache_f16, void* stream);
+
+/* kvb_stitch with a bf16 cache, fused with the per-layer deviation of the rows
+ * it stitches (Alg. 2 steps 1-2 in one pass: the stitched keys are compared
+ * with k_fresh while they are in registers instead of being read back).
+ * Stitch outputs (k_cache, v_cache, optional v_cache_f16) are bit-identical
+ * to kvb_stitch(..., KVB_BF16, ...).  For every row t of a chunk in the list
+ * and every layer l, delta[l][t] = 1 - (1/Hkv) sum_h cos(k_cache[l][h][t],
+ * k_fresh[l][h][t]) with cos as in kvb_deviation (double sums over the bf16
+ * values, the same zero-norm rule; the summation order differs, so values can
+ * differ from kvb_deviation's in the last float bit; identical rows still give
+ * 0 exactly).  K only, every layer its own set.  Rows outside the listed
+ * chunks (live rows, whose cache already holds the fresh values) are not
+ * written: kvb_select reads delta only at candidate rows, which are the
+ * stitched rows.  k_cache, v_cache, v_cache_f16, k_fresh bf16/fp16
+ * [L][Hkv][t_total][d]; delta f32 [L][t_total].
+ * Errors: as kvb_stitch; k_fresh and delta must be non-NULL and aligned. */
+kvb_status kvb_stitch_deviation(const kvb_pool_layout* pool, int32_t n_pool,
+                                const uint8_t* k_codes, const float* k_scale, const float* k_zero,
+                                const uint8_t* v_codes, const float* v_scale, const float* v_zero,
+                                const kvb_chunk* chunks, int32_t n_chunks,
+                                const float* rope_cos, const float* rope_sin, int64_t t_total,
+                                uint16_t* k_cache, uint16_t* v_cache, uint16_t* v_cache_f16,
+                                const uint16_t* k_fresh, float* delta, void* stream);
 
 /* Per-token deviation (Alg. 2 step 2):
  *   delta[s][t] = 1 - (1/N) * sum cos(cache[l][h][t], fresh[l][h][t])

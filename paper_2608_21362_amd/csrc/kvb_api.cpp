@@ -72,7 +72,7 @@ kvb_status check_pool(const kvb_pool_layout* p) {
 
 extern "C" {
 
-int kvb_abi_version(void) { return 2; }
+int kvb_abi_version(void) { return 3; }
 
 const char* kvb_last_error(void) { return g_err.c_str(); }
 
@@ -209,6 +209,33 @@ kvb_status kvb_stitch(const kvb_pool_layout* pool, int32_t n_pool, const uint8_t
                                        out_dtype, k_cache, v_cache, v_cache_f16,
                                        (hipStream_t)stream),
                     "kvb_stitch");
+}
+
+kvb_status kvb_stitch_deviation(const kvb_pool_layout* pool, int32_t n_pool,
+                                const uint8_t* k_codes, const float* k_scale, const float* k_zero,
+                                const uint8_t* v_codes, const float* v_scale, const float* v_zero,
+                                const kvb_chunk* chunks, int32_t n_chunks, const float* rope_cos,
+                                const float* rope_sin, int64_t t_total, uint16_t* k_cache,
+                                uint16_t* v_cache, uint16_t* v_cache_f16, const uint16_t* k_fresh,
+                                float* delta, void* stream) {
+  if (kvb_status s = check_pool(pool)) return s;
+  REQUIRE(n_pool > 0, "n_pool must be positive");
+  REQUIRE(n_chunks >= 0, "n_chunks < 0");
+  REQUIRE(t_total > 0 && t_total <= INT32_MAX, "t_total must be in (0, 2^31)");
+  REQUIRE(pool->n_layers <= 65535, "n_layers > 65535");
+  const void* ptrs[] = {k_codes, k_scale, k_zero, v_codes, v_scale, v_zero,
+                        k_cache, v_cache, k_fresh, delta};
+  for (const void* p : ptrs) REQUIRE(p != nullptr && aligned16(p), "null or misaligned tensor");
+  if (v_cache_f16) REQUIRE(aligned16(v_cache_f16), "misaligned fp16 shadow of V");
+  if (n_chunks == 0) return ok();
+  REQUIRE(chunks != nullptr && rope_cos != nullptr && rope_sin != nullptr,
+          "chunks and rotation tables are required");
+  REQUIRE(aligned16(rope_cos) && aligned16(rope_sin), "rotation tables must be 16-byte aligned");
+  return hip_status(kvb::launch_stitch_deviation(*pool, n_pool, k_codes, k_scale, k_zero, v_codes,
+                                                 v_scale, v_zero, chunks, n_chunks, rope_cos,
+                                                 rope_sin, t_total, k_cache, v_cache, v_cache_f16,
+                                                 k_fresh, delta, (hipStream_t)stream),
+                    "kvb_stitch_deviation");
 }
 
 static kvb_status check_deviation(int32_t n_layers, int32_t n_kv_heads, int32_t head_dim,

@@ -28,6 +28,16 @@ hipError_t launch_stitch(const kvb_pool_layout& p, int32_t n_pool, const uint8_t
                          int64_t t_total, kvb_dtype out_dtype, void* k_cache, void* v_cache,
                          uint16_t* v_cache_f16, hipStream_t s);
 
+// Stitch plus the per-layer K deviation of the stitched rows (bf16 cache).
+hipError_t launch_stitch_deviation(const kvb_pool_layout& p, int32_t n_pool,
+                                   const uint8_t* k_codes, const float* k_scale,
+                                   const float* k_zero, const uint8_t* v_codes,
+                                   const float* v_scale, const float* v_zero,
+                                   const kvb_chunk* chunks, int32_t n_chunks,
+                                   const float* rope_cos, const float* rope_sin, int64_t t_total,
+                                   void* k_cache, void* v_cache, uint16_t* v_cache_f16,
+                                   const uint16_t* k_fresh, float* delta, hipStream_t s);
+
 hipError_t launch_deviation(int n_layers, int n_kv_heads, int head_dim, int64_t t_total,
                             const uint16_t* k_cache, const uint16_t* k_fresh,
                             const uint16_t* v_cache, const uint16_t* v_fresh, int per_layer,

@@ -49,6 +49,9 @@ _SIGS = {
                                  _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "kvb_stitch": (_i32, [ctypes.POINTER(kvb_pool_layout), _i32, _vp, _vp, _vp, _vp, _vp, _vp,
                           _vp, _i32, _vp, _vp, _i64, _i32, _vp, _vp, _vp, _vp]),
+    "kvb_stitch_deviation": (_i32, [ctypes.POINTER(kvb_pool_layout), _i32, _vp, _vp, _vp, _vp,
+                                    _vp, _vp, _vp, _i32, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp,
+                                    _vp]),
     "kvb_deviation": (_i32, [_i32, _i32, _i32, _i64, _vp, _vp, _vp, _vp, _i32, _vp, _vp]),
     "kvb_select_workspace_bytes": (_sz, [_i32, _i64, _i32]),
     "kvb_select": (_i32, [_i32, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
@@ -162,6 +165,16 @@ def kvb_stitch(pool, n_pool, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero,
                            _p(v_codes), _p(v_scale), _p(v_zero), _p(chunks), n_chunks,
                            _p(rope_cos), _p(rope_sin), t_total, out_dtype, _p(k_cache),
                            _p(v_cache), _p(v_cache_f16), _stream(stream)))
+
+
+def kvb_stitch_deviation(pool, n_pool, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero,
+                         chunks, n_chunks, rope_cos, rope_sin, t_total, k_cache, v_cache,
+                         v_cache_f16, k_fresh, delta, stream=None):
+    _check(_lib.kvb_stitch_deviation(ctypes.byref(pool), n_pool, _p(k_codes), _p(k_scale),
+                                     _p(k_zero), _p(v_codes), _p(v_scale), _p(v_zero), _p(chunks),
+                                     n_chunks, _p(rope_cos), _p(rope_sin), t_total, _p(k_cache),
+                                     _p(v_cache), _p(v_cache_f16), _p(k_fresh), _p(delta),
+                                     _stream(stream)))
 
 
 def kvb_deviation(n_layers, n_kv_heads, head_dim, t_total, k_cache, k_fresh, v_cache, v_fresh,

@@ -196,6 +196,22 @@ def stitch(di: DeviceInputs, pb: PathBuffers, out_dtype=kvb.KVB_BF16, k_out=None
                    stream)
 
 
+def stitch_deviation(di: DeviceInputs, pb: PathBuffers, stream=None):
+    """Stitch (bf16 cache and fp16 shadow) fused with the per-layer deviation of
+    the stitched rows."""
+    kvb.kvb_stitch_deviation(di.pool, di.n_pool, di.k_codes, di.k_scale, di.k_zero, di.v_codes,
+                             di.v_scale, di.v_zero, di.chunks, di.n_pool, di.rope_cos,
+                             di.rope_sin, di.w.t_total, pb.k_cache, pb.v_cache, pb.v_cache_f16,
+                             di.k_fresh, pb.delta, stream)
+
+
+def select(di: DeviceInputs, pb: PathBuffers, stream=None):
+    """Row selection on pb.delta."""
+    kvb.kvb_select(di.n_sets, di.w.t_total, di.cu_seqlens, len(di.s.cu_seqlens) - 1, pb.delta,
+                   di.row_flags, di.k_per_set, pb.rows, pb.cu_rows, pb.sel_ws, pb.sel_ws_bytes,
+                   stream)
+
+
 def deviation(di: DeviceInputs, pb: PathBuffers, stream=None):
     """Deviation of the stitched K against the fresh K only (no selection)."""
     w = di.w

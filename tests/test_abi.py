@@ -33,7 +33,7 @@ def test_every_declared_symbol_is_exported():
     for n in names:
         assert hasattr(lib, n), n
     assert sorted(names) == sorted(kvb.EXPORTED)
-    assert kvb.kvb_abi_version() == 2
+    assert kvb.kvb_abi_version() == 3
 
 
 @pytest.mark.parametrize("theta,d", [(1e4, 64), (1e6, 128)])
@@ -114,6 +114,32 @@ def _stitch(**over):
 def test_stitch_rejects(over, status):
     with pytest.raises(kvb.KvbError) as e:
         _stitch(**over)
+    assert e.value.status == status
+
+
+def _stitch_dev(**over):
+    args = dict(pool=_pool(), n_pool=1, k_codes=FAKE, k_scale=FAKE, k_zero=FAKE, v_codes=FAKE,
+                v_scale=FAKE, v_zero=FAKE, chunks=FAKE, n_chunks=1, rope_cos=FAKE, rope_sin=FAKE,
+                t_total=128, k_cache=FAKE, v_cache=FAKE, v_cache_f16=None, k_fresh=FAKE,
+                delta=FAKE, stream=0)
+    args.update(over)
+    kvb.kvb_stitch_deviation(**args)
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(pool=_pool(bits=2)), kvb.KVB_EUNSUPPORTED),
+    (dict(pool=_pool(head_dim=96, v_group=32)), kvb.KVB_EUNSUPPORTED),
+    (dict(k_fresh=None), kvb.KVB_EINVAL),
+    (dict(delta=None), kvb.KVB_EINVAL),
+    (dict(delta=FAKE + 4), kvb.KVB_EINVAL),
+    (dict(k_cache=FAKE + 2), kvb.KVB_EINVAL),
+    (dict(v_cache_f16=FAKE + 2), kvb.KVB_EINVAL),
+    (dict(t_total=0), kvb.KVB_EINVAL),
+    (dict(rope_sin=None), kvb.KVB_EINVAL),
+])
+def test_stitch_deviation_rejects(over, status):
+    with pytest.raises(kvb.KvbError) as e:
+        _stitch_dev(**over)
     assert e.value.status == status
 
 

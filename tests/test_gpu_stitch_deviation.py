@@ -1,0 +1,131 @@
+"""GPU parity of kvb_stitch_deviation (stitch fused with the per-layer K
+deviation of the stitched rows) against the oracle and the unfused calls.
+
+* stitch outputs (K, V, fp16 shadow of V): bit-identical to kvb_stitch and to
+  the oracle's stitch;
+* delta at every stitched row and layer: within one float32 ulp of the
+  oracle's per-layer K deviation (float64) rounded to float32;
+* rows outside the stitched chunks (sinks, cache misses): delta untouched;
+* fresh keys equal to the stitched cache: delta exactly 0 on every stitched row;
+* selection on the fused deltas: equal to the oracle's selection, or differing
+  only inside the 1e-4 band at the cut.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import kvb_workload as kw
+from oracle import deviation as odev
+from oracle import populate as opop, selection as osel, stitch as ostitch
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    "tiny": kw.WORKLOADS["tiny"],
+    "qwen_1l": kw.WORKLOADS["qwen_1l"],
+    "int4_2l": kw.scaled(kw.WORKLOADS["qwen_36l_8k"], n_layers=2, chunks_per_prompt=9),
+    "sinks_seams_2l": kw.scaled(kw.WORKLOADS["long_32k"], n_layers=2, chunks_per_prompt=7),
+    "batched_small": kw.scaled(kw.WORKLOADS["batched_mixed"], n_prompts=3, chunks_per_prompt=5),
+}
+UNTOUCHED = -7.0  # delta sentinel for rows the fused call must not write
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _np16(t):
+    return t.detach().cpu().numpy().view(np.uint16)
+
+
+def _ulp32(x):
+    return np.spacing(np.abs(np.asarray(x, np.float32)))
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_stitch_deviation(name):
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2608_21362_amd import pipeline
+
+    w = CASES[name]
+    s = kw.structure(w)
+    _say(f"[stitch_deviation] {name}: L={w.n_layers} T={w.t_total}")
+    dev = pipeline.populate(w, s)
+    ref = opop.populate(w, s)
+    hit = s.hit_row
+    L, T = w.n_layers, w.t_total
+
+    # unfused stitch, for bitwise comparison
+    pu = pipeline.buffers(dev)
+    pipeline.stitch(dev, pu)
+    # fused call
+    pf = pipeline.buffers(dev)
+    pf.delta = torch.full((L, T), UNTOUCHED, dtype=torch.float32, device="cuda")
+    pipeline.stitch_deviation(dev, pf)
+    torch.cuda.synchronize()
+    for a, b, nm in ((pu.k_cache, pf.k_cache, "K"), (pu.v_cache, pf.v_cache, "V"),
+                     (pu.v_cache_f16, pf.v_cache_f16, "fp16 V")):
+        assert torch.equal(a, b), f"{name}: fused {nm} differs from kvb_stitch"
+
+    # oracle: stitch, then the per-layer K deviation
+    ck, cv = ref.cache_k.copy(), ref.cache_v.copy()
+    ostitch.stitch_into(ck, cv, ref.pool, ref.chunks, ref.cos, ref.sin, "bf16")
+    assert np.array_equal(_np16(pf.k_cache), ck) and np.array_equal(_np16(pf.v_cache), cv)
+    rd32 = odev.deviation(ck, ref.k_fresh, per_layer=True).astype(np.float32)
+    gd = pf.delta.cpu().numpy()
+    assert np.all(np.abs(gd[:, hit].astype(np.float64) - rd32[:, hit]) <= _ulp32(rd32[:, hit])), \
+        f"{name}: fused deviation beyond 1 ulp"
+    assert np.all(gd[:, ~hit] == UNTOUCHED), f"{name}: a row outside the chunks was written"
+    _say(f"[stitch_deviation] {name}: {float(np.mean(gd[:, hit] == rd32[:, hit])):.6f} of stitched "
+         f"rows bit-equal to the oracle; {int((~hit).sum())} live rows untouched")
+
+    # selection on the fused deltas (live rows are never candidates)
+    if w.per_layer or L == 1:
+        forced = osel.forced_rows(s.cu_seqlens, hit, s.chunk_starts, w.seam_left, w.seam_right)
+        kseq = osel.k_per_prompt(s.cu_seqlens, hit, w.rho_num, w.rho_den)
+        pipeline.select(dev, pf)
+        torch.cuda.synchronize()
+        rows, cu = pf.rows.cpu().numpy(), pf.cu_rows.cpu().numpy()
+        for li in range(L):
+            ref_d = rd32[li].copy()
+            ref_d[~hit] = UNTOUCHED
+            r_rows, r_cu = osel.select(ref_d, hit, forced, s.cu_seqlens, kseq)
+            g_rows = rows[li, : cu[li, -1]]
+            assert np.all(np.diff(g_rows) > 0)
+            if np.array_equal(g_rows, r_rows) and np.array_equal(cu[li], r_cu):
+                continue
+            diff = np.setxor1d(g_rows, r_rows)
+            for b in range(len(s.cu_seqlens) - 1):
+                lo, hi = s.cu_seqlens[b], s.cu_seqlens[b + 1]
+                cand = [r for r in range(lo, hi) if hit[r]]
+                order = osel.top_k(ref_d, cand, len(cand))
+                k = int(kseq[b])
+                d_b = diff[(diff >= lo) & (diff < hi)]
+                if len(d_b) and 0 < k < len(order):
+                    kth = float(ref_d[order[k - 1]])
+                    assert np.all(np.abs(ref_d[d_b].astype(np.float64) - kth) <= 1e-4)
+
+
+@pytest.mark.parametrize("name", ["tiny", "int4_2l"])
+def test_identical_rows_give_zero(name):
+    """Fresh keys set to the stitched cache: every stitched row has delta = 0
+    exactly (dot and both norms are summed in one order)."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2608_21362_amd import pipeline
+
+    w = CASES[name]
+    s = kw.structure(w)
+    dev = pipeline.populate(w, s)
+    pb = pipeline.buffers(dev)
+    pipeline.stitch(dev, pb)
+    torch.cuda.synchronize()
+    dev.k_fresh.copy_(pb.k_cache)
+    pb.delta = torch.full((w.n_layers, w.t_total), UNTOUCHED, dtype=torch.float32, device="cuda")
+    pipeline.stitch_deviation(dev, pb)
+    torch.cuda.synchronize()
+    gd = pb.delta.cpu().numpy()
+    assert np.all(gd[:, s.hit_row] == 0.0), f"{name}: identical rows do not give delta = 0"
