@@ -610,6 +610,7 @@ __device__ __forceinline__ void build_plan(
     int32_t n_wg, int32_t n_first, int32_t n_wg_max, int32_t* __restrict__ plan) {
   __shared__ int warp_sums[16];
   __shared__ int carry_sh;
+  __shared__ int prefix_sh[2 * kAttnMaxWorkgroups + 1];  // balanced ranges: n_tiles < 2 n_wg
   int32_t* prefix = plan + 4;
   int32_t* first = plan + 5 + n_tiles;
   int4* meta = reinterpret_cast<int4*>(plan + tile_meta_offset(n_tiles, n_wg_max));
@@ -645,7 +646,10 @@ __device__ __forceinline__ void build_plan(
     __syncthreads();
     int before = carry_sh;
     for (int i = 0; i < wv; ++i) before += warp_sums[i];
-    if (t < n_tiles) prefix[t] = before + x - nb;
+    if (t < n_tiles) {
+      prefix[t] = before + x - nb;
+      prefix_sh[t] = before + x - nb;
+    }
     __syncthreads();
     if (tid == nt - 1) carry_sh = before + x;
     __syncthreads();
@@ -661,13 +665,14 @@ __device__ __forceinline__ void build_plan(
     plan[2] = n_first;
     plan[3] = total;
     prefix[n_tiles] = total;
+    prefix_sh[n_tiles] = total;
   }
   __syncthreads();
   // tile holding unit unit_start(w): every non-empty tile [p0, p1) writes the
   // workgroups whose first unit lies in it (one pass, no search); workgroups
   // that start past the last unit get n_tiles (they have no work)
   for (int t = tid; t < n_tiles; t += nt) {
-    const int p0 = prefix[t], p1 = prefix[t + 1];
+    const int p0 = prefix_sh[t], p1 = prefix_sh[t + 1];
     if (p1 <= p0) continue;
     for (int w = unit_owner(p0, c1, c2, n_first); w < n_wg; ++w) {
       const int u = unit_start(w, c1, c2, n_first);
