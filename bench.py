@@ -262,6 +262,25 @@ def main():
             b.record(stream)
             torch.cuda.synchronize()
             acc.append(a.elapsed_time(b))
+    # chunk importance (cache population, Sec. 4.4; not part of the step): fp32
+    # keys of every pool chunk and layer, cache flushed before each repetition
+    from paper_2608_21362_amd import kvb as _kvb
+    P = di.n_pool
+    k_pool = torch.randn((P, L, w.n_kv_heads, w.chunk_len, w.head_dim), dtype=torch.float32,
+                         device="cuda")
+    imp = torch.zeros(P, dtype=torch.float64, device="cuda")
+    imp_f = []
+    for _ in range(5):
+        flush.sum()
+        a, b = ev(), ev()
+        a.record(stream)
+        _kvb.kvb_chunk_importance(di.pool, P, L, _kvb.KVB_F32, k_pool, imp)
+        b.record(stream)
+        torch.cuda.synchronize()
+        imp_f.append(a.elapsed_time(b))
+    imp_bytes = k_pool.numel() * 4 + P * 8
+    imp_gbs = imp_bytes / (np.median(imp_f) * 1e-3) / 1e9
+    del k_pool, imp
     del flush
     st_gbs = st_bytes / (np.median(st_f) * 1e-3) / 1e9
     dv_gbs = dev_bytes / (np.median(dv_f) * 1e-3) / 1e9
@@ -324,6 +343,9 @@ def main():
             "stitch_deviation_GBps_flushed": sd_gbs, "stitch_deviation_hbm_frac": sd_gbs / HBM_PEAK_GBS,
             "stitch_deviation_bytes": sd_bytes,
             "deviation_bytes": dev_bytes,
+            "chunk_importance_GBps_flushed": imp_gbs,
+            "chunk_importance_hbm_frac": imp_gbs / HBM_PEAK_GBS,
+            "chunk_importance_bytes": int(imp_bytes),
             "selected_rows_per_layer": float(np.mean(cu[:, -1])),
         },
     }

@@ -18,7 +18,7 @@
  *
  * plus the host helpers that prepare their inputs (rotation tables, row
  * flags) and the cache-population kernels (RoPE at absolute positions, KIVI
- * quantisation; Sec. 4.6 warm).
+ * quantisation, chunk importance; Sec. 4.6 warm, Sec. 4.4).
  *
  * Conventions
  *   - Every pointer named as a tensor, descriptor, index or workspace is a
@@ -87,7 +87,7 @@ typedef struct {
 
 /* 3 for this header (version 2 added the optional fp16 shadow of V to
  * kvb_stitch, kvb_sparse_attn and kvb_sparse_attn_workspace_bytes; version 3
- * added kvb_stitch_deviation). */
+ * added kvb_stitch_deviation and kvb_chunk_importance). */
 int kvb_abi_version(void);
 
 /* Thread-local message of the last failing call on this thread. */
@@ -154,6 +154,23 @@ kvb_status kvb_kivi_quantize(const kvb_pool_layout* pool, int32_t n_pool, int32_
                              int32_t n_in, kvb_dtype in_dtype, const void* k_in, const void* v_in,
                              uint8_t* k_codes, float* k_scale, float* k_zero,
                              uint8_t* v_codes, float* v_scale, float* v_zero, void* stream);
+
+/* Chunk importance for the cache manager's eviction order (Sec. 4.4, the
+ * importance equation): importance(C) = 1/(L Hkv C) sum over layers, kv heads
+ * and tokens of the chunk of ||k||_2, the mean Euclidean norm of its cached key
+ * vectors.  k_in: in_dtype (F32 or F64) [n_pool][n_in][Hkv][C][d], n_in of the
+ * pool's L layers (the keys as cached, e.g. the same input kvb_kivi_quantize
+ * takes); importance: f64 [n_pool], ACCUMULATED: every call adds its layers'
+ * share (sum of their norms / (L Hkv C)), so calls over disjoint layer sets
+ * starting from zero leave the mean over all layers.  Double arithmetic; the
+ * order of the sums is fixed (deterministic), so it can differ from a plain
+ * left-to-right sum in the last bits.  For callers that rank chunks for
+ * eviction; not part of the timed path.
+ * Errors: KVB_EINVAL, KVB_EUNSUPPORTED (head_dim, bits, chunk_len as in
+ * kvb_pool_layout). */
+kvb_status kvb_chunk_importance(const kvb_pool_layout* pool, int32_t n_pool, int32_t n_in,
+                                kvb_dtype in_dtype, const void* k_in, double* importance,
+                                void* stream);
 
 /* ---- the hot path ------------------------------------------------------- */
 

@@ -18,7 +18,7 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from . import kivi, numerics, rope
+from . import importance, kivi, numerics, rope
 
 SENTINEL_BF16 = np.uint16(0xFFFF)  # a NaN pattern no stitched value can take
 
@@ -36,6 +36,7 @@ class Populated:
     cache_v: np.ndarray
     noise_rows: list      # per populated layer, bool [T]
     layers: list
+    importance: np.ndarray = None  # float64 [P]: chunk importance over the populated layers
 
 
 def _rotate_pool_keys(k_pool_raw, src_pos, theta):
@@ -74,11 +75,13 @@ def populate(w, s, layers=None, draws_fn=None, with_q=True) -> Populated:
     q = np.zeros((Lp, T, w.n_q_heads, d), np.uint16) if with_q else None
     pos = s.positions()
     noise = []
+    imp = np.zeros(P, np.float64)
     for i, l in enumerate(layers):
         dr = draws_fn(l)
         noise.append(dr.noise_rows)
         if P:
             k_rot = _rotate_pool_keys(dr.k_pool_raw, s.src_pos, w.rope_theta)
+            imp += importance.layer_share(k_rot[:, None], Lp)
             kc, ks, kz = kivi.quantise_keys(k_rot, w.bits, w.k_group)
             vc, vs, vz = kivi.quantise_values(dr.v_pool_raw, w.bits, w.v_group)
             pool["k_codes"][:, i] = kivi.pack(kc, w.bits)
@@ -98,4 +101,4 @@ def populate(w, s, layers=None, draws_fn=None, with_q=True) -> Populated:
     cos, sin = rope.angle_table(w.rope_theta, d, s.dst_pos.astype(np.int64) - s.src_pos)
     return Populated(pool=pool, chunks=chunks, cos=cos, sin=sin, k_fresh=k_fresh,
                      v_fresh=v_fresh, q=q, cache_k=cache_k, cache_v=cache_v,
-                     noise_rows=noise, layers=layers)
+                     noise_rows=noise, layers=layers, importance=imp)

@@ -182,6 +182,22 @@ kvb_status kvb_kivi_quantize(const kvb_pool_layout* pool, int32_t n_pool, int32_
                     "kvb_kivi_quantize");
 }
 
+kvb_status kvb_chunk_importance(const kvb_pool_layout* pool, int32_t n_pool, int32_t n_in,
+                                kvb_dtype in_dtype, const void* k_in, double* importance,
+                                void* stream) {
+  if (kvb_status s = check_pool(pool)) return s;
+  REQUIRE(n_pool > 0 && n_pool <= INT32_MAX / 2, "n_pool must be positive");
+  REQUIRE(n_in > 0 && n_in <= pool->n_layers, "n_in must be in [1, n_layers]");
+  REQUIRE(in_dtype == KVB_F32 || in_dtype == KVB_F64, "in_dtype must be F32 or F64");
+  REQUIRE((int64_t)n_in * pool->n_kv_heads * pool->chunk_len <= INT32_MAX,
+          "too many key vectors per chunk");
+  REQUIRE(k_in != nullptr && aligned16(k_in), "null or misaligned key tensor");
+  REQUIRE(importance != nullptr && aligned16(importance), "null or misaligned importance");
+  return hip_status(kvb::launch_chunk_importance(*pool, n_pool, n_in, in_dtype, k_in, importance,
+                                                 (hipStream_t)stream),
+                    "kvb_chunk_importance");
+}
+
 kvb_status kvb_stitch(const kvb_pool_layout* pool, int32_t n_pool, const uint8_t* k_codes,
                       const float* k_scale, const float* k_zero, const uint8_t* v_codes,
                       const float* v_scale, const float* v_zero, const kvb_chunk* chunks,

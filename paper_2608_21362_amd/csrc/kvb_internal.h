@@ -19,6 +19,9 @@ hipError_t launch_kivi_quantize(const kvb_pool_layout& p, int32_t n_pool, int32_
                                 int32_t n_in, kvb_dtype in_dtype, const void* k_in,
                                 const void* v_in, uint8_t* k_codes, float* k_scale, float* k_zero,
                                 uint8_t* v_codes, float* v_scale, float* v_zero, hipStream_t s);
+hipError_t launch_chunk_importance(const kvb_pool_layout& p, int32_t n_pool, int32_t n_in,
+                                   kvb_dtype in_dtype, const void* k_in, double* importance,
+                                   hipStream_t s);
 
 // ---- hot path -------------------------------------------------------------
 hipError_t launch_stitch(const kvb_pool_layout& p, int32_t n_pool, const uint8_t* k_codes,

@@ -1,6 +1,7 @@
-// Cache population kernels: RoPE at absolute positions (Eq. 3) and KIVI
-// quantisation of cached chunks (Sec. 4.5, Eq. 7).  These prepare the chunk
-// pool and the probe-pass tensors; they are not timed as part of the path.
+// Cache population kernels: RoPE at absolute positions (Eq. 3), KIVI
+// quantisation of cached chunks (Sec. 4.5, Eq. 7) and the chunks' importance
+// for the eviction order (Sec. 4.4).  These prepare the chunk pool and the
+// probe-pass tensors; they are not timed as part of the path.
 #include <math.h>
 
 #include "kvb_device.h"
@@ -230,6 +231,51 @@ hipError_t launch_rope_rows(int head_dim, int64_t n_outer, int64_t n_rows, int64
   return hipGetLastError();
 }
 
+// Chunk importance (Sec. 4.4): one workgroup per chunk; lane i of wave w takes
+// the chunk's key vectors w*64 + i, w*64 + i + 1024, ... whole: it reads each
+// vector with 16-byte loads, sums its squares in channel order (double) and
+// adds the norm to its running sum.  The lanes' sums are combined with a fixed
+// xor-shuffle tree, the 16 wave sums in wave order, and the chunk's share is
+// added to importance[p].  Fixed assignment and order: deterministic.
+template <typename T>
+__device__ __forceinline__ double sum_sq4(const void* p, int64_t i) {  // i: multiple of 4
+  if constexpr (sizeof(T) == 8) {
+    const double2 a = *reinterpret_cast<const double2*>(reinterpret_cast<const double*>(p) + i);
+    const double2 b = *reinterpret_cast<const double2*>(reinterpret_cast<const double*>(p) + i + 2);
+    return __builtin_fma(b.y, b.y, __builtin_fma(b.x, b.x, __builtin_fma(a.y, a.y, a.x * a.x)));
+  } else {
+    const float4 a = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p) + i);
+    const double x0 = a.x, x1 = a.y, x2 = a.z, x3 = a.w;
+    return __builtin_fma(x3, x3, __builtin_fma(x2, x2, __builtin_fma(x1, x1, x0 * x0)));
+  }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(1024)
+importance_kernel(int32_t n_vectors, int32_t D, double inv_count, const void* __restrict__ in,
+                  double* __restrict__ importance) {
+  __shared__ double wave_sum[16];
+  const int p = blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t base = (int64_t)p * n_vectors * D;
+  double acc = 0.0;
+  for (int v = threadIdx.x; v < n_vectors; v += 1024) {
+    const int64_t row = base + (int64_t)v * D;
+    double ss = 0.0;
+    for (int j = 0; j < D; j += 4) ss += sum_sq4<T>(in, row + j);
+    acc += sqrt(ss);
+  }
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) acc += __shfl_xor(acc, m, 64);
+  if (lane == 0) wave_sum[wave] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double total = 0.0;
+    for (int w = 0; w < 16; ++w) total += wave_sum[w];
+    importance[p] += total * inv_count;
+  }
+}
+
 hipError_t launch_kivi_quantize(const kvb_pool_layout& p, int32_t n_pool, int32_t first_layer,
                                 int32_t n_in, kvb_dtype in_dtype, const void* k_in,
                                 const void* v_in, uint8_t* k_codes, float* k_scale, float* k_zero,
@@ -251,6 +297,20 @@ hipError_t launch_kivi_quantize(const kvb_pool_layout& p, int32_t n_pool, int32_
                        p.n_layers, first_layer, n_in, p.n_kv_heads, p.chunk_len, p.head_dim,
                        p.bits, p.v_group, v_in, v_codes, v_scale, v_zero);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_chunk_importance(const kvb_pool_layout& p, int32_t n_pool, int32_t n_in,
+                                   kvb_dtype in_dtype, const void* k_in, double* importance,
+                                   hipStream_t s) {
+  const int32_t n_vectors = n_in * p.n_kv_heads * p.chunk_len;
+  const double inv_count = 1.0 / ((double)p.n_layers * p.n_kv_heads * p.chunk_len);
+  if (in_dtype == KVB_F64)
+    hipLaunchKernelGGL(importance_kernel<double>, dim3(n_pool), dim3(1024), 0, s, n_vectors,
+                       p.head_dim, inv_count, k_in, importance);
+  else
+    hipLaunchKernelGGL(importance_kernel<float>, dim3(n_pool), dim3(1024), 0, s, n_vectors,
+                       p.head_dim, inv_count, k_in, importance);
   return hipGetLastError();
 }
 

@@ -47,6 +47,8 @@ _SIGS = {
     "kvb_rope_rows": (_i32, [_i32, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp]),
     "kvb_kivi_quantize": (_i32, [ctypes.POINTER(kvb_pool_layout), _i32, _i32, _i32, _i32, _vp, _vp,
                                  _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "kvb_chunk_importance": (_i32, [ctypes.POINTER(kvb_pool_layout), _i32, _i32, _i32, _vp, _vp,
+                                    _vp]),
     "kvb_stitch": (_i32, [ctypes.POINTER(kvb_pool_layout), _i32, _vp, _vp, _vp, _vp, _vp, _vp,
                           _vp, _i32, _vp, _vp, _i64, _i32, _vp, _vp, _vp, _vp]),
     "kvb_stitch_deviation": (_i32, [ctypes.POINTER(kvb_pool_layout), _i32, _vp, _vp, _vp, _vp,
@@ -157,6 +159,11 @@ def kvb_kivi_quantize(pool, n_pool, first_layer, n_in, in_dtype, k_in, v_in, k_c
 
 
 # ---- the hot path -------------------------------------------------------------
+
+def kvb_chunk_importance(pool, n_pool, n_in, in_dtype, k_in, importance, stream=None):
+    _check(_lib.kvb_chunk_importance(ctypes.byref(pool), n_pool, n_in, in_dtype, _p(k_in),
+                                     _p(importance), _stream(stream)))
+
 
 def kvb_stitch(pool, n_pool, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, chunks,
                n_chunks, rope_cos, rope_sin, t_total, out_dtype, k_cache, v_cache, v_cache_f16,

@@ -57,6 +57,7 @@ class DeviceInputs:
     max_seq_len: int
     host_flags: np.ndarray = field(default=None)
     host_k: np.ndarray = field(default=None)
+    importance: Optional[torch.Tensor] = None  # f64 [P]: chunk importance (Sec. 4.4)
 
     @property
     def n_layers(self):
@@ -96,6 +97,7 @@ def populate(w: kw.Workload, s: kw.Structure, layers=None, with_q=True, draws_fn
     u_d = _dev(np.arange(C, dtype=np.int32))
     outer_src = _dev(np.repeat(s.src_pos.astype(np.int32), H)) if P else None
     k_rot = torch.empty((P, H, C, d), dtype=torch.float64, **dev) if P else None
+    importance = torch.zeros(max(P, 1), dtype=torch.float64, **dev)
     for i, l in enumerate(layers):
         dr = draws_fn(l)
         if P:
@@ -105,6 +107,7 @@ def populate(w: kw.Workload, s: kw.Structure, layers=None, with_q=True, draws_fn
                               kvb.KVB_F64, k_rot)
             kvb.kvb_kivi_quantize(pool, P, i, 1, kvb.KVB_F64, k_rot, vp.double(), k_codes,
                                   k_scale, k_zero, v_codes, v_scale, v_zero)
+            kvb.kvb_chunk_importance(pool, P, 1, kvb.KVB_F64, k_rot, importance)
         kr = _dev(dr.k_raw)
         kvb.kvb_rope_rows(d, H, T, 1, kr, pos_d, None, tab_c, tab_s, max_pos, kvb.KVB_BF16,
                           k_fresh[i])
@@ -138,7 +141,8 @@ def populate(w: kw.Workload, s: kw.Structure, layers=None, with_q=True, draws_fn
         v_fresh=v_fresh, q=q, cache_init_k=cache_k, cache_init_v=cache_v,
         cu_seqlens=_dev(s.cu_seqlens.astype(np.int32)), row_flags=_dev(flags),
         k_per_set=_dev(np.tile(kseq[None, :], (n_sets, 1)).astype(np.int32)),
-        max_rows=max_rows, max_seq_len=max_seq_len, host_flags=flags, host_k=kseq)
+        max_rows=max_rows, max_seq_len=max_seq_len, host_flags=flags, host_k=kseq,
+        importance=importance[:P])
 
 
 @dataclass

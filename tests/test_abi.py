@@ -212,6 +212,21 @@ def test_sparse_attn_rejects(over, status):
     assert e.value.status == status
 
 
+def test_chunk_importance_rejects():
+    with pytest.raises(kvb.KvbError) as e:
+        kvb.kvb_chunk_importance(_pool(), 1, 1, kvb.KVB_BF16, FAKE, FAKE, 0)
+    assert e.value.status == kvb.KVB_EINVAL
+    with pytest.raises(kvb.KvbError):
+        kvb.kvb_chunk_importance(_pool(), 1, 2, kvb.KVB_F64, FAKE, FAKE, 0)  # n_in > n_layers
+    with pytest.raises(kvb.KvbError):
+        kvb.kvb_chunk_importance(_pool(), 1, 1, kvb.KVB_F64, None, FAKE, 0)
+    with pytest.raises(kvb.KvbError):
+        kvb.kvb_chunk_importance(_pool(), 1, 1, kvb.KVB_F64, FAKE, FAKE + 8, 0)
+    with pytest.raises(kvb.KvbError) as e:
+        kvb.kvb_chunk_importance(_pool(head_dim=96, v_group=32), 1, 1, kvb.KVB_F64, FAKE, FAKE, 0)
+    assert e.value.status == kvb.KVB_EUNSUPPORTED
+
+
 def test_population_rejects():
     with pytest.raises(kvb.KvbError) as e:
         kvb.kvb_rope_rows(96, 1, 1, 1, FAKE, FAKE, None, FAKE, FAKE, 10, kvb.KVB_BF16, FAKE, 0)

@@ -48,7 +48,9 @@ def _np16(t):
 
 
 # Small cases: several tiles of every kernel, a ragged tail, both code widths,
-# both head sizes, sinks, seams, several prompts and several layers.
+# both head sizes, sinks, seams, several prompts and several layers, and the
+# paper's method variants (all-layer deviation, SelectiveRecompute alone,
+# rho = 0.25).
 SMALL = {
     "tiny": kw.WORKLOADS["tiny"],
     "qwen_1l": kw.WORKLOADS["qwen_1l"],
@@ -57,6 +59,11 @@ SMALL = {
     "batched_small": kw.scaled(kw.WORKLOADS["batched_mixed"], n_prompts=3, chunks_per_prompt=5),
     "all_layer_delta": kw.scaled(kw.WORKLOADS["qwen_36l_8k"], n_layers=3, chunks_per_prompt=4,
                                  per_layer=False, seam_left=16, seam_right=0),
+    # method variants: SelectiveRecompute alone (Alg. 1 one-sided windows, no
+    # top-k) and a larger recompute fraction (rho = 0.25)
+    "selective_only": kw.scaled(kw.WORKLOADS["qwen_1l"], rho_num=0, seam_left=16, seam_right=0),
+    "rho25_2l": kw.scaled(kw.WORKLOADS["qwen_36l_8k"], n_layers=2, chunks_per_prompt=6,
+                          rho_num=25),
 }
 
 
@@ -113,6 +120,19 @@ def test_population_bitexact(name):
     assert np.array_equal(_np16(d.k_fresh), r.k_fresh)
     assert np.array_equal(_np16(d.v_fresh), r.v_fresh)
     assert np.array_equal(_np16(d.q), r.q)
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_chunk_importance(name):
+    """Chunk importance (Sec. 4.4) accumulated layer by layer during
+    population: double sums in a fixed order, against the oracle's mean."""
+    c = case(name)
+    g = c.dev.importance.cpu().numpy()
+    r = c.ref.importance
+    assert g.shape == r.shape
+    np.testing.assert_allclose(g, r, rtol=1e-12, atol=0)
+    # the eviction order the scores induce is the oracle's
+    assert np.array_equal(np.argsort(g, kind="stable"), np.argsort(r, kind="stable"))
 
 
 @pytest.mark.parametrize("name", list(SMALL))
