@@ -151,7 +151,8 @@ def main():
     log(f"[bench] workload {w.name}: L={w.n_layers} T={w.t_total} chunks={s.n_pool} "
         f"bits={w.bits}; populating on the GPU")
     t0 = time.time()
-    di = pipeline.populate(w, s)
+    di = pipeline.populate(w, s, progress=lambda i, n: log(f"[bench] populated {i}/{n} layers")
+                           if i % 6 == 0 or i == n else None)
     pb = pipeline.buffers(di, attn_all_layers=args.attn_all_layers)
     torch.cuda.synchronize()
     log(f"[bench] inputs resident ({time.time() - t0:.1f} s)")

@@ -68,8 +68,10 @@ class DeviceInputs:
         return self.n_layers if self.w.per_layer else 1
 
 
-def populate(w: kw.Workload, s: kw.Structure, layers=None, with_q=True, draws_fn=None) -> DeviceInputs:
-    """Upload the raw draws and build pool / fresh tensors on the GPU."""
+def populate(w: kw.Workload, s: kw.Structure, layers=None, with_q=True, draws_fn=None,
+             progress=None) -> DeviceInputs:
+    """Upload the raw draws and build pool / fresh tensors on the GPU.
+    ``progress(i, n)``, if given, is called after each populated layer."""
     layers = list(range(w.n_layers)) if layers is None else list(layers)
     if draws_fn is None:
         def draws_fn(l):
@@ -118,6 +120,8 @@ def populate(w: kw.Workload, s: kw.Structure, layers=None, with_q=True, draws_fn
             kvb.kvb_rope_rows(d, 1, T, Hq, qr, pos_d, None, tab_c, tab_s, max_pos, kvb.KVB_BF16,
                               q[i])
         torch.cuda.synchronize()
+        if progress is not None:
+            progress(i + 1, len(layers))
     chunks_np = np.stack([np.arange(P), s.src_pos, s.dst_row, s.dst_pos], axis=1).astype(np.int32)
     rc, rs = kvb.kvb_rope_delta_table(w.rope_theta, d, (s.dst_pos - s.src_pos).astype(np.int32))
     hit = torch.from_numpy(s.hit_row).cuda()
