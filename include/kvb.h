@@ -85,9 +85,10 @@ typedef struct {
   int32_t pool_idx, src_pos, dst_row, dst_pos;
 } kvb_chunk;
 
-/* 3 for this header (version 2 added the optional fp16 shadow of V to
+/* 4 for this header (version 2 added the optional fp16 shadow of V to
  * kvb_stitch, kvb_sparse_attn and kvb_sparse_attn_workspace_bytes; version 3
- * added kvb_stitch_deviation and kvb_chunk_importance). */
+ * added kvb_stitch_deviation and kvb_chunk_importance; version 4 added
+ * kvb_probe_gate). */
 int kvb_abi_version(void);
 
 /* Thread-local message of the last failing call on this thread. */
@@ -123,6 +124,25 @@ kvb_status kvb_row_flags(int32_t n_seqs, const int32_t* cu_seqlens, int32_t n_si
                          int32_t chunk_len, const kvb_chunk* chunks, int32_t n_chunks,
                          int32_t seam_left, int32_t seam_right, int32_t rho_num, int32_t rho_den,
                          uint8_t* row_flags, int32_t* k_per_seq);
+
+/* Threshold-activated probe (Sec. 7.4: the probe pass costs time in
+ * proportion to the cached tokens and can be skipped when the hit ratio is
+ * below a minimum; HOST only, no GPU).  For prompt b with n_b candidate rows
+ * (row_flags bit KVB_ROW_CANDIDATE) out of T_b rows, the probe runs iff
+ * n_b > 0 and n_b * min_den >= min_num * T_b (64-bit integers, exact).  A
+ * prompt without the probe has no deviation to rank: k_per_seq[b] is set to 0,
+ * so kvb_select keeps only its forced rows (live rows and seam windows,
+ * SelectiveRecompute alone); the other entries are left as they are.
+ * *n_probed (optional, NULL for none) receives the number of probed prompts;
+ * with 0 the caller can skip the deviation pass altogether (kvb_stitch
+ * instead of kvb_stitch_deviation, then kvb_select: the deviations of
+ * prompts with k = 0 are never read).  min_num = 0 keeps every prompt that
+ * has a candidate.  cu_seqlens [n_seqs+1], row_flags [t_total], k_per_seq
+ * [n_seqs] (in/out): all HOST.  Errors: KVB_EINVAL (null pointer, n_seqs <= 0,
+ * min_den <= 0, min_num < 0, cu_seqlens not starting at 0 or decreasing). */
+kvb_status kvb_probe_gate(int32_t n_seqs, const int32_t* cu_seqlens, const uint8_t* row_flags,
+                          int32_t min_num, int32_t min_den, int32_t* k_per_seq,
+                          int32_t* n_probed);
 
 /* ---- cache population (Sec. 4.6 warm, Sec. 4.5, Eq. 3) ----------------- */
 
@@ -185,7 +205,9 @@ kvb_status kvb_chunk_importance(const kvb_pool_layout* pool, int32_t n_pool, int
  * k_cache / v_cache: [L][Hkv][t_total][d] of out_dtype (KVB_BF16 or KVB_F32);
  * only rows of the listed chunks are written -- live rows (misses, sinks) are
  * the caller's.  Chunks must not overlap.  A chunk whose pool_idx or rows fall
- * outside the arrays is skipped.  n_pool bounds pool_idx.
+ * outside the arrays is skipped.  n_pool bounds pool_idx; n_pool = 0 (nothing
+ * cached: a cold prompt) is allowed with n_chunks = 0 and then the pool arrays
+ * may be NULL (the call returns KVB_OK and writes nothing).
  * v_cache_f16 (optional, NULL for none; bf16 caches only): fp16 shadow of
  * v_cache, same layout; the stitched V rows are also stored there as the fp16
  * value of their bf16 result (exact while |v| <= 65504 and v is not below the
@@ -213,7 +235,8 @@ kvb_status kvb_stitch(const kvb_pool_layout* pool, int32_t n_pool,
  * written: kvb_select reads delta only at candidate rows, which are the
  * stitched rows.  k_cache, v_cache, v_cache_f16, k_fresh bf16/fp16
  * [L][Hkv][t_total][d]; delta f32 [L][t_total].
- * Errors: as kvb_stitch; k_fresh and delta must be non-NULL and aligned. */
+ * Errors: as kvb_stitch (also the empty-pool rule); k_fresh and delta must be
+ * non-NULL and aligned. */
 kvb_status kvb_stitch_deviation(const kvb_pool_layout* pool, int32_t n_pool,
                                 const uint8_t* k_codes, const float* k_scale, const float* k_zero,
                                 const uint8_t* v_codes, const float* v_scale, const float* v_zero,

@@ -42,7 +42,7 @@ class Workload:
     v_group: int           # Gv: channels per value-statistic group (values are per token)
     n_prompts: int
     chunks_per_prompt: int
-    placement: str         # "permuted" | "identity" | "half_hits"
+    placement: str         # "permuted" | "identity" | "half_hits" | "prefix_hits" | "ramp_hits"
     n_sinks: int = 0
     seam_left: int = 0     # rows before each chunk boundary forced into the recompute set
     seam_right: int = 0    # rows after each chunk boundary forced into the recompute set
@@ -56,6 +56,11 @@ class Workload:
     max_src_pos: int = 32768
     seed: int = 0
     chunk_len: int = 128
+    hit_chunks: int = 0    # "prefix_hits": the first hit_chunks chunks of each prompt are cached
+    # threshold-activated probe: a prompt whose cached fraction of rows is below
+    # probe_min_num / probe_min_den skips the deviation pass (its top-k is empty)
+    probe_min_num: int = 0
+    probe_min_den: int = 100
 
     @property
     def prompt_len(self) -> int:
@@ -167,6 +172,19 @@ def structure(w: Workload) -> Structure:
         elif w.placement == "identity":
             offs = rng.integers(0, w.max_src_pos, size=w.chunks_per_prompt)
             for i in range(w.chunks_per_prompt):
+                p = int(chunk_pos[i])
+                src.append(int(offs[i]))
+                dst_pos.append(p)
+                dst_row.append(base + p)
+        elif w.placement in ("prefix_hits", "ramp_hits"):
+            # a reused context: its leading chunks were cached at random offsets
+            # ("ramp_hits": prompt b has floor(b * chunks / n_prompts) of them)
+            if w.placement == "prefix_hits":
+                n_hit = min(w.hit_chunks, w.chunks_per_prompt)
+            else:
+                n_hit = b * w.chunks_per_prompt // w.n_prompts
+            offs = rng.integers(0, w.max_src_pos, size=n_hit)
+            for i in range(n_hit):
                 p = int(chunk_pos[i])
                 src.append(int(offs[i]))
                 dst_pos.append(p)

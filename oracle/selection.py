@@ -52,6 +52,31 @@ def k_per_prompt(cu_seqlens, candidate, rho_num: int, rho_den: int) -> np.ndarra
     return np.asarray(ks, dtype=np.int64)
 
 
+def probe_gate(cu_seqlens, candidate, k_per_seq, min_num: int, min_den: int):
+    """Threshold-activated probe (Sec. 7.4, "Limitations": the probe pass costs
+    time in proportion to the cached tokens and can be skipped when the cache
+    hit ratio is below a minimum).
+
+    Readings: the hit ratio of prompt b is n_b / T_b, its candidate (cached)
+    rows over all its rows; the probe runs for prompt b iff n_b > 0 and
+    n_b * min_den >= min_num * T_b (integers, so the comparison is exact); a
+    prompt without the probe has no deviation to rank, so its top-k is empty
+    (k_b = 0) and only its forced rows -- live rows and seam windows, i.e.
+    SelectiveRecompute alone -- are recomputed.
+
+    Returns (k_per_seq with the skipped prompts' k set to 0, bool [B] probed).
+    """
+    k = np.array(k_per_seq, dtype=np.int64, copy=True)
+    probed = np.zeros(len(cu_seqlens) - 1, dtype=bool)
+    for b in range(len(cu_seqlens) - 1):
+        lo, hi = int(cu_seqlens[b]), int(cu_seqlens[b + 1])
+        n = int(np.count_nonzero(candidate[lo:hi]))
+        probed[b] = n > 0 and n * min_den >= min_num * (hi - lo)
+        if not probed[b]:
+            k[b] = 0
+    return k, probed
+
+
 def _rank_key(value: float, row: int):
     """Sort key: numbers by value descending (-0 as +0), then NaN; row ascending
     within equal keys."""

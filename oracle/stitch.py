@@ -51,7 +51,10 @@ def stitch_into(cache_k, cache_v, pool, chunks, cos, sin, out_dtype: str, layers
     """Write the stitched rows into caches [len(layers)][Hkv][T][d].
 
     ``out_dtype`` "f32": caches are float32 arrays; "bf16": caches hold uint16
-    bfloat16 bit patterns.  Rows outside the chunks are left untouched."""
+    bfloat16 bit patterns.  Rows outside the chunks are left untouched; with no
+    chunk (nothing cached) nothing is written."""
+    if np.asarray(chunks).shape[0] == 0:
+        return
     k, v = stitch_values(pool, chunks, cos, sin, layers)
     C = k.shape[3]
     for c in range(k.shape[0]):

@@ -72,7 +72,7 @@ kvb_status check_pool(const kvb_pool_layout* p) {
 
 extern "C" {
 
-int kvb_abi_version(void) { return 3; }
+int kvb_abi_version(void) { return 4; }
 
 const char* kvb_last_error(void) { return g_err.c_str(); }
 
@@ -141,6 +141,31 @@ kvb_status kvb_row_flags(int32_t n_seqs, const int32_t* cu_seqlens, int32_t n_si
   return ok();
 }
 
+kvb_status kvb_probe_gate(int32_t n_seqs, const int32_t* cu_seqlens, const uint8_t* row_flags,
+                          int32_t min_num, int32_t min_den, int32_t* k_per_seq,
+                          int32_t* n_probed) {
+  REQUIRE(n_seqs > 0, "n_seqs must be positive");
+  REQUIRE_PTR(cu_seqlens);
+  REQUIRE_PTR(row_flags);
+  REQUIRE_PTR(k_per_seq);
+  REQUIRE(min_den > 0 && min_num >= 0, "the minimum hit ratio is min_num / min_den, min_den > 0");
+  REQUIRE(cu_seqlens[0] == 0, "cu_seqlens[0] must be 0");
+  for (int32_t b = 0; b < n_seqs; ++b)
+    REQUIRE(cu_seqlens[b + 1] >= cu_seqlens[b], "cu_seqlens must be non-decreasing");
+  int32_t probed = 0;
+  for (int32_t b = 0; b < n_seqs; ++b) {
+    const int64_t lo = cu_seqlens[b], hi = cu_seqlens[b + 1];
+    int64_t n_cand = 0;
+    for (int64_t r = lo; r < hi; ++r) n_cand += (row_flags[r] & KVB_ROW_CANDIDATE) ? 1 : 0;
+    if (n_cand > 0 && n_cand * min_den >= (int64_t)min_num * (hi - lo))
+      ++probed;
+    else
+      k_per_seq[b] = 0;
+  }
+  if (n_probed) *n_probed = probed;
+  return ok();
+}
+
 kvb_status kvb_rope_rows(int32_t head_dim, int64_t n_outer, int64_t n_rows, int64_t n_inner,
                          const float* x, const int32_t* row_pos, const int32_t* outer_pos,
                          const float* table_cos, const float* table_sin, int32_t table_len,
@@ -205,13 +230,15 @@ kvb_status kvb_stitch(const kvb_pool_layout* pool, int32_t n_pool, const uint8_t
                       int64_t t_total, kvb_dtype out_dtype, void* k_cache, void* v_cache,
                       uint16_t* v_cache_f16, void* stream) {
   if (kvb_status s = check_pool(pool)) return s;
-  REQUIRE(n_pool > 0, "n_pool must be positive");
-  REQUIRE(n_chunks >= 0, "n_chunks < 0");
+  REQUIRE(n_pool >= 0 && n_chunks >= 0, "n_pool and n_chunks must be non-negative");
+  REQUIRE(n_pool > 0 || n_chunks == 0, "chunks listed with an empty pool");
   REQUIRE(t_total > 0 && t_total <= INT32_MAX, "t_total must be in (0, 2^31)");
   REQUIRE(out_dtype == KVB_BF16 || out_dtype == KVB_F32, "out_dtype must be BF16 or F32");
   REQUIRE((int64_t)pool->n_layers * pool->n_kv_heads <= 65535, "n_layers * n_kv_heads > 65535");
-  const void* ptrs[] = {k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, k_cache, v_cache};
-  for (const void* p : ptrs) REQUIRE(p != nullptr && aligned16(p), "null or misaligned tensor");
+  const void* ptrs[] = {k_cache, v_cache, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero};
+  // an empty pool (nothing cached) may come with NULL pool arrays
+  for (size_t i = 0; i < (n_pool > 0 ? 8u : 2u); ++i)
+    REQUIRE(ptrs[i] != nullptr && aligned16(ptrs[i]), "null or misaligned tensor");
   if (v_cache_f16) {
     REQUIRE(out_dtype == KVB_BF16, "an fp16 shadow of V goes with a bf16 cache");
     REQUIRE(aligned16(v_cache_f16), "misaligned fp16 shadow of V");
@@ -235,13 +262,15 @@ kvb_status kvb_stitch_deviation(const kvb_pool_layout* pool, int32_t n_pool,
                                 uint16_t* v_cache, uint16_t* v_cache_f16, const uint16_t* k_fresh,
                                 float* delta, void* stream) {
   if (kvb_status s = check_pool(pool)) return s;
-  REQUIRE(n_pool > 0, "n_pool must be positive");
-  REQUIRE(n_chunks >= 0, "n_chunks < 0");
+  REQUIRE(n_pool >= 0 && n_chunks >= 0, "n_pool and n_chunks must be non-negative");
+  REQUIRE(n_pool > 0 || n_chunks == 0, "chunks listed with an empty pool");
   REQUIRE(t_total > 0 && t_total <= INT32_MAX, "t_total must be in (0, 2^31)");
   REQUIRE(pool->n_layers <= 65535, "n_layers > 65535");
-  const void* ptrs[] = {k_codes, k_scale, k_zero, v_codes, v_scale, v_zero,
-                        k_cache, v_cache, k_fresh, delta};
-  for (const void* p : ptrs) REQUIRE(p != nullptr && aligned16(p), "null or misaligned tensor");
+  const void* ptrs[] = {k_cache, v_cache, k_fresh, delta, k_codes,
+                        k_scale, k_zero,  v_codes, v_scale, v_zero};
+  // an empty pool (nothing cached) may come with NULL pool arrays
+  for (size_t i = 0; i < (n_pool > 0 ? 10u : 4u); ++i)
+    REQUIRE(ptrs[i] != nullptr && aligned16(ptrs[i]), "null or misaligned tensor");
   if (v_cache_f16) REQUIRE(aligned16(v_cache_f16), "misaligned fp16 shadow of V");
   if (n_chunks == 0) return ok();
   REQUIRE(chunks != nullptr && rope_cos != nullptr && rope_sin != nullptr,

@@ -44,6 +44,7 @@ _SIGS = {
     "kvb_last_error": (ctypes.c_char_p, []),
     "kvb_rope_delta_table": (_i32, [_f64, _i32, _vp, _i32, _vp, _vp]),
     "kvb_row_flags": (_i32, [_i32, _vp, _i32, _i32, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp]),
+    "kvb_probe_gate": (_i32, [_i32, _vp, _vp, _i32, _i32, _vp, _vp]),
     "kvb_rope_rows": (_i32, [_i32, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp]),
     "kvb_kivi_quantize": (_i32, [ctypes.POINTER(kvb_pool_layout), _i32, _i32, _i32, _i32, _vp, _vp,
                                  _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
@@ -140,6 +141,16 @@ def kvb_row_flags(cu_seqlens, n_sinks, chunk_len, chunks, seam_left, seam_right,
     _check(_lib.kvb_row_flags(n_seqs, _p(cu), n_sinks, chunk_len, _p(ch), ch.shape[0], seam_left,
                               seam_right, rho_num, rho_den, _p(flags), _p(k)))
     return flags, k
+
+
+def kvb_probe_gate(cu_seqlens, row_flags, k_per_seq, min_num, min_den):
+    """Returns (k_per_seq with skipped prompts at 0, number of probed prompts)."""
+    cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+    fl = np.ascontiguousarray(row_flags, dtype=np.uint8)
+    k = np.array(k_per_seq, dtype=np.int32, copy=True)
+    n = np.zeros(1, np.int32)
+    _check(_lib.kvb_probe_gate(cu.shape[0] - 1, _p(cu), _p(fl), min_num, min_den, _p(k), _p(n)))
+    return k, int(n[0])
 
 
 # ---- population ---------------------------------------------------------------

@@ -58,6 +58,7 @@ class DeviceInputs:
     host_flags: np.ndarray = field(default=None)
     host_k: np.ndarray = field(default=None)
     importance: Optional[torch.Tensor] = None  # f64 [P]: chunk importance (Sec. 4.4)
+    n_probed: int = 0  # prompts whose deviation pass runs (threshold-activated probe)
 
     @property
     def n_layers(self):
@@ -130,6 +131,8 @@ def populate(w: kw.Workload, s: kw.Structure, layers=None, with_q=True, draws_fn
     cache_v = torch.where(hit[None, None, :, None], sentinel, v_fresh)
     flags, kseq = kvb.kvb_row_flags(s.cu_seqlens, w.n_sinks, C, chunks_np, w.seam_left,
                                     w.seam_right, w.rho_num, w.rho_den)
+    kseq, n_probed = kvb.kvb_probe_gate(s.cu_seqlens, flags, kseq, w.probe_min_num,
+                                        w.probe_min_den)
     n_sets = L if w.per_layer else 1
     forced = (flags & kvb.KVB_ROW_FORCED) != 0
     bound = 0
@@ -146,7 +149,7 @@ def populate(w: kw.Workload, s: kw.Structure, layers=None, with_q=True, draws_fn
         cu_seqlens=_dev(s.cu_seqlens.astype(np.int32)), row_flags=_dev(flags),
         k_per_set=_dev(np.tile(kseq[None, :], (n_sets, 1)).astype(np.int32)),
         max_rows=max_rows, max_seq_len=max_seq_len, host_flags=flags, host_k=kseq,
-        importance=importance[:P])
+        importance=importance[:P], n_probed=n_probed)
 
 
 @dataclass
@@ -262,9 +265,13 @@ def sparse_attn_all(di: DeviceInputs, pb: PathBuffers, out_dtype=kvb.KVB_BF16, s
 
 def run_path(di: DeviceInputs, pb: PathBuffers, attn_all_layers=False, out_dtype=kvb.KVB_BF16,
              stream=None):
-    """One pass of the whole path over the batch."""
+    """One pass of the whole path over the batch.  With no prompt above the
+    probe threshold the deviation pass is skipped (every top-k is empty)."""
     stitch(di, pb, stream=stream)
-    deviation_topk(di, pb, stream=stream)
+    if di.n_probed:
+        deviation_topk(di, pb, stream=stream)
+    else:
+        select(di, pb, stream=stream)
     if attn_all_layers:
         sparse_attn_all(di, pb, out_dtype, stream)
     else:

@@ -33,7 +33,7 @@ def test_every_declared_symbol_is_exported():
     for n in names:
         assert hasattr(lib, n), n
     assert sorted(names) == sorted(kvb.EXPORTED)
-    assert kvb.kvb_abi_version() == 3
+    assert kvb.kvb_abi_version() == 4
 
 
 @pytest.mark.parametrize("theta,d", [(1e4, 64), (1e6, 128)])
@@ -110,11 +110,23 @@ def _stitch(**over):
     (dict(rope_cos=None), kvb.KVB_EINVAL),
     (dict(v_cache_f16=FAKE + 2), kvb.KVB_EINVAL),
     (dict(v_cache_f16=FAKE, out_dtype=kvb.KVB_F32), kvb.KVB_EINVAL),  # shadow needs a bf16 cache
+    (dict(n_pool=0), kvb.KVB_EINVAL),                  # chunks listed with an empty pool
+    (dict(n_pool=-1, n_chunks=0), kvb.KVB_EINVAL),
+    (dict(n_pool=0, n_chunks=0, k_cache=None), kvb.KVB_EINVAL),
 ])
 def test_stitch_rejects(over, status):
     with pytest.raises(kvb.KvbError) as e:
         _stitch(**over)
     assert e.value.status == status
+
+
+def test_empty_pool_is_a_no_op():
+    """A cold prompt: nothing cached, no chunks, NULL pool arrays.  Both stitch
+    entry points return before any device work (no GPU needed)."""
+    empty = dict(n_pool=0, n_chunks=0, k_codes=None, k_scale=None, k_zero=None, v_codes=None,
+                 v_scale=None, v_zero=None, chunks=None, rope_cos=None, rope_sin=None)
+    _stitch(**empty)
+    _stitch_dev(**empty)
 
 
 def _stitch_dev(**over):
@@ -136,6 +148,8 @@ def _stitch_dev(**over):
     (dict(v_cache_f16=FAKE + 2), kvb.KVB_EINVAL),
     (dict(t_total=0), kvb.KVB_EINVAL),
     (dict(rope_sin=None), kvb.KVB_EINVAL),
+    (dict(n_pool=0), kvb.KVB_EINVAL),
+    (dict(n_pool=0, n_chunks=0, delta=None), kvb.KVB_EINVAL),
 ])
 def test_stitch_deviation_rejects(over, status):
     with pytest.raises(kvb.KvbError) as e:

@@ -50,7 +50,8 @@ def _np16(t):
 # Small cases: several tiles of every kernel, a ragged tail, both code widths,
 # both head sizes, sinks, seams, several prompts and several layers, and the
 # paper's method variants (all-layer deviation, SelectiveRecompute alone,
-# rho = 0.25).
+# rho = 0.25, the threshold-activated probe) and the two request kinds of the
+# synthetic trace.
 SMALL = {
     "tiny": kw.WORKLOADS["tiny"],
     "qwen_1l": kw.WORKLOADS["qwen_1l"],
@@ -64,6 +65,22 @@ SMALL = {
     "selective_only": kw.scaled(kw.WORKLOADS["qwen_1l"], rho_num=0, seam_left=16, seam_right=0),
     "rho25_2l": kw.scaled(kw.WORKLOADS["qwen_36l_8k"], n_layers=2, chunks_per_prompt=6,
                           rho_num=25),
+    # request shapes of the synthetic trace: a warm request whose leading chunks
+    # were cached at random offsets, and a cold one (nothing cached, every row live)
+    "prefix_hits_2l": kw.scaled(kw.WORKLOADS["qwen_36l_8k"], n_layers=2, chunks_per_prompt=7,
+                                placement="prefix_hits", hit_chunks=3, seam_left=16,
+                                seam_right=16),
+    "cold_2l": kw.scaled(kw.WORKLOADS["qwen_36l_8k"], n_layers=2, chunks_per_prompt=3,
+                         placement="prefix_hits", hit_chunks=0, seam_left=16, seam_right=16),
+    # threshold-activated probe: prompts cache 0, 1, 3 and 4 of 6 chunks; the
+    # last two reach 40 % and are probed, the others keep only forced rows
+    "probe_gate_4p": kw.scaled(kw.WORKLOADS["qwen_36l_8k"], n_layers=2, n_prompts=4,
+                               chunks_per_prompt=6, placement="ramp_hits", seam_left=16,
+                               seam_right=16, probe_min_num=40, probe_min_den=100),
+    # no prompt reaches the threshold: the deviation pass is skipped
+    "probe_off_3p": kw.scaled(kw.WORKLOADS["qwen_36l_8k"], n_layers=1, n_prompts=3,
+                              chunks_per_prompt=5, placement="ramp_hits", seam_left=16,
+                              probe_min_num=1, probe_min_den=1),
 }
 
 
@@ -96,6 +113,8 @@ class Case:
         self.forced = osel.forced_rows(self.s.cu_seqlens, self.s.hit_row, self.s.chunk_starts,
                                        w.seam_left, w.seam_right)
         self.kseq = osel.k_per_prompt(self.s.cu_seqlens, cand, w.rho_num, w.rho_den)
+        self.kseq, self.probed = osel.probe_gate(self.s.cu_seqlens, cand, self.kseq,
+                                                 w.probe_min_num, w.probe_min_den)
 
     def gpu_layer(self, i):
         return self.layers[i]
@@ -172,9 +191,15 @@ def test_deviation_and_selection(name):
     gd = c.pb.delta.cpu().numpy()
     rd32 = c.ref_delta.astype(np.float32)
     assert gd.shape == rd32.shape
-    assert np.all(np.abs(gd.astype(np.float64) - rd32) <= _ulp32(rd32)), "deviation beyond 1 ulp"
-    exact = float(np.mean(gd == rd32))
-    _say(f"[deviation] {name}: {exact:.6f} of rows bit-equal to the oracle")
+    assert c.dev.n_probed == int(c.probed.sum())
+    if c.dev.n_probed == 0:
+        # no prompt reaches the probe threshold: the deviation pass is skipped
+        assert np.all(gd == 0), "deviation written although no prompt is probed"
+    else:
+        assert np.all(np.abs(gd.astype(np.float64) - rd32) <= _ulp32(rd32)), \
+            "deviation beyond 1 ulp"
+        exact = float(np.mean(gd == rd32))
+        _say(f"[deviation] {name}: {exact:.6f} of rows bit-equal to the oracle")
     rows = c.pb.rows.cpu().numpy()
     cu = c.pb.cu_rows.cpu().numpy()
     for si in range(gd.shape[0]):

@@ -28,6 +28,12 @@ CASES = {
     "int4_2l": kw.scaled(kw.WORKLOADS["qwen_36l_8k"], n_layers=2, chunks_per_prompt=9),
     "sinks_seams_2l": kw.scaled(kw.WORKLOADS["long_32k"], n_layers=2, chunks_per_prompt=7),
     "batched_small": kw.scaled(kw.WORKLOADS["batched_mixed"], n_prompts=3, chunks_per_prompt=5),
+    "prefix_hits_2l": kw.scaled(kw.WORKLOADS["qwen_36l_8k"], n_layers=2, chunks_per_prompt=7,
+                                placement="prefix_hits", hit_chunks=3, seam_left=16,
+                                seam_right=16),
+    # nothing cached: the fused call is a no-op (no row is written)
+    "cold_2l": kw.scaled(kw.WORKLOADS["qwen_36l_8k"], n_layers=2, chunks_per_prompt=3,
+                         placement="prefix_hits", hit_chunks=0, seam_left=16, seam_right=16),
 }
 UNTOUCHED = -7.0  # delta sentinel for rows the fused call must not write
 
@@ -79,8 +85,9 @@ def test_stitch_deviation(name):
     assert np.all(np.abs(gd[:, hit].astype(np.float64) - rd32[:, hit]) <= _ulp32(rd32[:, hit])), \
         f"{name}: fused deviation beyond 1 ulp"
     assert np.all(gd[:, ~hit] == UNTOUCHED), f"{name}: a row outside the chunks was written"
-    _say(f"[stitch_deviation] {name}: {float(np.mean(gd[:, hit] == rd32[:, hit])):.6f} of stitched "
-         f"rows bit-equal to the oracle; {int((~hit).sum())} live rows untouched")
+    same = float(np.mean(gd[:, hit] == rd32[:, hit])) if hit.any() else 1.0
+    _say(f"[stitch_deviation] {name}: {same:.6f} of stitched rows bit-equal to the oracle; "
+         f"{int((~hit).sum())} live rows untouched")
 
     # selection on the fused deltas (live rows are never candidates)
     if w.per_layer or L == 1:
