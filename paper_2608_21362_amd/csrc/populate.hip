@@ -231,39 +231,55 @@ hipError_t launch_rope_rows(int head_dim, int64_t n_outer, int64_t n_rows, int64
   return hipGetLastError();
 }
 
-// Chunk importance (Sec. 4.4): one workgroup per chunk; lane i of wave w takes
-// the chunk's key vectors w*64 + i, w*64 + i + 1024, ... whole: it reads each
-// vector with 16-byte loads, sums its squares in channel order (double) and
-// adds the norm to its running sum.  The lanes' sums are combined with a fixed
-// xor-shuffle tree, the 16 wave sums in wave order, and the chunk's share is
-// added to importance[p].  Fixed assignment and order: deterministic.
+// Chunk importance (Sec. 4.4): one workgroup of 1024 lanes per chunk.  Each key
+// vector is read by 8 adjacent lanes: 16-byte piece i of the vector goes to
+// lane i % 8, so every load instruction of a wave reads 8 whole 128-byte
+// segments (8 vectors).  All of a lane's pieces are requested before any is
+// summed; a lane sums its squares in piece order (double), the 8 lanes combine
+// theirs with a fixed xor tree (every level adds two values, so all 8 end with
+// the same bits), and the vector's first lane adds the norm to its running
+// sum.  The lanes' sums are combined with a fixed xor-shuffle tree, the 16 wave
+// sums in wave order, and the chunk's share is added to importance[p].  Fixed
+// assignment and order: deterministic.
+constexpr int kImpLanes = 8;  // lanes per key vector
+
 template <typename T>
-__device__ __forceinline__ double sum_sq4(const void* p, int64_t i) {  // i: multiple of 4
+__device__ __forceinline__ double sum_sq_piece(const T* p) {  // one 16-byte piece
   if constexpr (sizeof(T) == 8) {
-    const double2 a = *reinterpret_cast<const double2*>(reinterpret_cast<const double*>(p) + i);
-    const double2 b = *reinterpret_cast<const double2*>(reinterpret_cast<const double*>(p) + i + 2);
-    return __builtin_fma(b.y, b.y, __builtin_fma(b.x, b.x, __builtin_fma(a.y, a.y, a.x * a.x)));
+    const double2 a = *reinterpret_cast<const double2*>(p);
+    return __builtin_fma(a.y, a.y, a.x * a.x);
   } else {
-    const float4 a = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p) + i);
+    const float4 a = *reinterpret_cast<const float4*>(p);
     const double x0 = a.x, x1 = a.y, x2 = a.z, x3 = a.w;
     return __builtin_fma(x3, x3, __builtin_fma(x2, x2, __builtin_fma(x1, x1, x0 * x0)));
   }
 }
 
-template <typename T>
+template <typename T, int D>
 __global__ void __launch_bounds__(1024)
-importance_kernel(int32_t n_vectors, int32_t D, double inv_count, const void* __restrict__ in,
+importance_kernel(int32_t n_vectors, double inv_count, const void* __restrict__ in,
                   double* __restrict__ importance) {
+  constexpr int PER = 16 / (int)sizeof(T);    // elements per piece
+  constexpr int NP = D / PER;                 // pieces per vector
+  constexpr int LP = NP / kImpLanes;          // pieces per lane
+  static_assert(LP >= 1 && NP % kImpLanes == 0, "a vector spans whole pieces of every lane");
   __shared__ double wave_sum[16];
   const int p = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t base = (int64_t)p * n_vectors * D;
+  const int sub = threadIdx.x % kImpLanes;
+  const T* base = reinterpret_cast<const T*>(in) + (int64_t)p * n_vectors * D;
   double acc = 0.0;
-  for (int v = threadIdx.x; v < n_vectors; v += 1024) {
-    const int64_t row = base + (int64_t)v * D;
+  for (int v = threadIdx.x / kImpLanes; v < n_vectors; v += 1024 / kImpLanes) {
+    const T* row = base + (int64_t)v * D + sub * PER;
+    double part[LP];
+#pragma unroll
+    for (int j = 0; j < LP; ++j) part[j] = sum_sq_piece<T>(row + j * kImpLanes * PER);
     double ss = 0.0;
-    for (int j = 0; j < D; j += 4) ss += sum_sq4<T>(in, row + j);
-    acc += sqrt(ss);
+#pragma unroll
+    for (int j = 0; j < LP; ++j) ss += part[j];
+#pragma unroll
+    for (int m = 1; m < kImpLanes; m <<= 1) ss += __shfl_xor(ss, m, 64);
+    if (sub == 0) acc += sqrt(ss);
   }
 #pragma unroll
   for (int m = 1; m < 64; m <<= 1) acc += __shfl_xor(acc, m, 64);
@@ -305,12 +321,15 @@ hipError_t launch_chunk_importance(const kvb_pool_layout& p, int32_t n_pool, int
                                    hipStream_t s) {
   const int32_t n_vectors = n_in * p.n_kv_heads * p.chunk_len;
   const double inv_count = 1.0 / ((double)p.n_layers * p.n_kv_heads * p.chunk_len);
-  if (in_dtype == KVB_F64)
-    hipLaunchKernelGGL(importance_kernel<double>, dim3(n_pool), dim3(1024), 0, s, n_vectors,
-                       p.head_dim, inv_count, k_in, importance);
-  else
-    hipLaunchKernelGGL(importance_kernel<float>, dim3(n_pool), dim3(1024), 0, s, n_vectors,
-                       p.head_dim, inv_count, k_in, importance);
+#define KVB_IMPORTANCE(T, D)                                                                    \
+  hipLaunchKernelGGL((importance_kernel<T, D>), dim3(n_pool), dim3(1024), 0, s, n_vectors,      \
+                     inv_count, k_in, importance)
+  if (in_dtype == KVB_F64) {
+    if (p.head_dim == 128) KVB_IMPORTANCE(double, 128); else KVB_IMPORTANCE(double, 64);
+  } else {
+    if (p.head_dim == 128) KVB_IMPORTANCE(float, 128); else KVB_IMPORTANCE(float, 64);
+  }
+#undef KVB_IMPORTANCE
   return hipGetLastError();
 }
 
