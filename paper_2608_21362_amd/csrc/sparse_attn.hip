@@ -5,7 +5,7 @@
 //   patch_kernel     cache[l][h][t] <- fresh[l][h][t] for every selected row t
 //                    (both tensors, every kv head), plus the fp16 image of the
 //                    new V rows when the caller keeps an fp16 shadow of V; its
-//                    last workgroup builds the work decomposition when the
+//                    first workgroup builds the work decomposition when the
 //                    launch uses balanced ranges (below)
 //   v16_kernel       only without a shadow: V of the call converted to fp16 in
 //                    the workspace (exact for |v| <= 65504: a bf16 significand
@@ -686,7 +686,7 @@ __device__ __forceinline__ void build_plan(
 
 // Patch: cache[l][h][t] <- fresh[l][h][t] for every selected row t (both
 // tensors, every kv head; one wave per row), with the fp16 image of the new V
-// rows when the caller keeps an fp16 shadow of V.  With plan != NULL the last
+// rows when the caller keeps an fp16 shadow of V.  With plan != NULL the first
 // workgroup builds the work decomposition instead.
 __global__ void __launch_bounds__(256)
 patch_kernel(int32_t L, int32_t Hkv, int32_t D, int64_t t_total, int32_t n_seqs,
@@ -697,12 +697,15 @@ patch_kernel(int32_t L, int32_t Hkv, int32_t D, int64_t t_total, int32_t n_seqs,
              const int32_t* __restrict__ cu_seqlens, int32_t n_tiles, int32_t tile_slots,
              int32_t rows_per_tile, int32_t n_wg, int32_t n_first, int32_t n_wg_max,
              int32_t* __restrict__ plan) {
-  if (plan != nullptr && blockIdx.x == gridDim.x - 1) {
+  // the plan builder is workgroup 0: dispatched first, it starts its chain of
+  // dependent loads while the copying workgroups are still being dispatched
+  if (plan != nullptr && blockIdx.x == 0) {
     build_plan(n_tiles, tile_slots, Hkv, t_total, cu_seqlens, n_seqs, rows, cu_rows,
                rows_per_layer, rows_per_tile, n_wg, n_first, n_wg_max, plan);
     return;
   }
-  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t copy_block = (int64_t)blockIdx.x - (plan != nullptr ? 1 : 0);
+  const int64_t wave = (copy_block * blockDim.x + threadIdx.x) >> 6;
   const int lane = threadIdx.x & 63;
   const int64_t l = wave / max_rows;
   const int64_t i = wave % max_rows;
