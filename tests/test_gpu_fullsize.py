@@ -1,8 +1,10 @@
 """Full-size GPU parity: the 36-layer 8K workload on every layer, the batched
 16 x 2048 workload, and three layers of the 36-layer 32K workload at their
-full per-layer size, in the launch configuration bench.py times (one stitch
-and one deviation + selection for all populated layers, then one attention
-call per layer with the fp16 shadow of V).
+full per-layer size, in the launch configuration bench.py times (one fused
+stitch + deviation and one selection for all populated layers, then one
+attention call per layer with the fp16 shadow of V); the 8K workload also in
+bench.py's --unfused configuration (one stitch, then one deviation +
+selection).
 
 Checks per layer, against the oracle built from the same seeded draws:
 stitch bit-exact (K, V and the fp16 shadow of the stitched V), deviation
@@ -44,16 +46,19 @@ def _ulp32(x):
 
 
 CASES = [
-    # name, GPU-populated layers (None = all), attention sample per layer, full layers
-    ("qwen_36l_8k", None, 256, "ends"),
-    ("batched_mixed", None, 1024, ""),
-    ("long_32k", [0, 17, 35], 256, ""),
+    # name, GPU-populated layers (None = all), attention sample per layer, full
+    # layers, fused stitch + deviation
+    ("qwen_36l_8k", None, 256, "ends", True),
+    ("batched_mixed", None, 1024, "", True),
+    ("long_32k", [0, 17, 35], 256, "", True),
+    ("qwen_36l_8k", None, 128, "", False),
 ]
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("name,layers,n_sample,full", CASES, ids=[c[0] for c in CASES])
-def test_fullsize(name, layers, n_sample, full):
+@pytest.mark.parametrize("name,layers,n_sample,full,fused", CASES,
+                         ids=[c[0] + ("" if c[4] else "_unfused") for c in CASES])
+def test_fullsize(name, layers, n_sample, full, fused):
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     from paper_2608_21362_amd import pipeline
@@ -62,12 +67,19 @@ def test_fullsize(name, layers, n_sample, full):
     s = kw.structure(w)
     gl = list(range(w.n_layers)) if layers is None else list(layers)
     L, T = len(gl), w.t_total
-    _say(f"[fullsize] {name}: layers {gl[0]}..{gl[-1]} ({L}) T={T}")
+    _say(f"[fullsize] {name} ({'fused' if fused else 'unfused'}): layers {gl[0]}..{gl[-1]} "
+         f"({L}) T={T}")
     dev = pipeline.populate(w, s, layers=gl)
     pb = pipeline.buffers(dev)
-    pipeline.stitch(dev, pb)
-    st_k, st_v, st_v16 = pb.k_cache.clone(), pb.v_cache.clone(), pb.v_cache_f16.clone()
-    pipeline.deviation_topk(dev, pb)
+    if fused:
+        # deviations of live rows stay at the buffer's zeros, which is their value
+        pipeline.stitch_deviation(dev, pb)
+        st_k, st_v, st_v16 = pb.k_cache.clone(), pb.v_cache.clone(), pb.v_cache_f16.clone()
+        pipeline.select(dev, pb)
+    else:
+        pipeline.stitch(dev, pb)
+        st_k, st_v, st_v16 = pb.k_cache.clone(), pb.v_cache.clone(), pb.v_cache_f16.clone()
+        pipeline.deviation_topk(dev, pb)
     for i in range(L):
         pipeline.sparse_attn_layer(dev, pb, i)
     torch.cuda.synchronize()
@@ -92,7 +104,14 @@ def test_fullsize(name, layers, n_sample, full):
         # deviation
         rd32 = odev.deviation(ck, ref.k_fresh, per_layer=True)[0].astype(np.float32)
         gd = delta[i]
-        assert np.all(np.abs(gd.astype(np.float64) - rd32) <= _ulp32(rd32)), f"layer {l}: deviation"
+        if fused:
+            # the fused call writes the stitched rows only; live rows keep 0
+            assert np.all(np.abs(gd[hit].astype(np.float64) - rd32[hit]) <= _ulp32(rd32[hit])), \
+                f"layer {l}: deviation"
+            assert np.all(gd[~hit] == 0.0), f"layer {l}: a live row's deviation was written"
+        else:
+            assert np.all(np.abs(gd.astype(np.float64) - rd32) <= _ulp32(rd32)), \
+                f"layer {l}: deviation"
         # selection: equal, or differing only inside the 1e-4 band at the cut
         g_rows = rows_all[i, : cu_all[i, -1]]
         r_rows, r_cu = osel.select(rd32, hit, forced, s.cu_seqlens, kseq)
