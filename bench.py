@@ -58,6 +58,9 @@ def algorithmic(w, s, rows_per_set, cu_rows_per_set):
     n_sets = rows_per_set.shape[0]
     dev_bytes = 2 * L * H * T * d * 2 + n_sets * T * 4
     fused_bytes = stitch_bytes + P * L * H * C * d * 2 + L * P * C * 4
+    # bytes read of each (the rest is written), for the practical ceilings
+    algorithmic.reads = {"stitch": codes + stats, "deviation": 2 * L * H * T * d * 2,
+                         "stitch_deviation": codes + stats + P * L * H * C * d * 2}
     pos = s.positions().astype(np.int64)
     flops_per_layer = []
     for l in range(L):
@@ -114,6 +117,72 @@ def cpu_baseline(w, s, n_layers_sample):
                   f"scaled to {w.n_layers} layers",
         "seconds": dt,
     }
+
+
+def measure_ceilings(torch):
+    """Practical ceilings on this device, next to the published peaks: a loop of
+    back-to-back bf16 32x32x16 matrix products in the attention kernel's launch
+    shape (no memory traffic), streaming read and copy kernels (16-byte
+    accesses) and torch's fill as the write stream, over 1 GiB.  Best of three
+    timed runs after one warm-up."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2608_21362_amd", "lib", "libkvb_ceiling.so"))
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    lib.kvb_ceiling_mfma.argtypes = [i32, i32, vp, vp]
+    lib.kvb_ceiling_read.argtypes = [vp, i64, i32, vp, vp]
+    lib.kvb_ceiling_copy.argtypes = [vp, vp, i64, i32, vp]
+    stream = torch.cuda.current_stream()
+    sh = ctypes.c_void_p(stream.cuda_stream)
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+
+    def best(fn, reps=3):
+        fn()
+        times = []
+        for _ in range(reps):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(b) * 1e-3)
+        return min(times)
+
+    def check(rc):
+        if rc != 0:
+            raise RuntimeError(f"ceiling kernel launch failed ({rc})")
+
+    n_wg, iters = 2 * n_cu, 4000
+    sink = torch.empty(n_wg * 256, dtype=torch.float32, device="cuda")
+    t = best(lambda: check(lib.kvb_ceiling_mfma(n_wg, iters, vp(sink.data_ptr()), sh)))
+    mfma_tflops = n_wg * 4 * iters * 8 * 32768 / t / 1e12
+    nbytes = 1 << 30
+    buf = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    rsink = torch.empty(8 * n_cu * 256, dtype=torch.int32, device="cuda")
+    t = best(lambda: check(lib.kvb_ceiling_read(vp(buf.data_ptr()), nbytes, 8 * n_cu,
+                                                 vp(rsink.data_ptr()), sh)))
+    read_gbs = nbytes / t / 1e9
+    half = nbytes // 2
+    t = best(lambda: check(lib.kvb_ceiling_copy(vp(buf.data_ptr()), vp(buf.data_ptr() + half),
+                                                 half, 8 * n_cu, sh)))
+    copy_gbs = 2 * half / t / 1e9
+    t = best(lambda: buf.fill_(3))
+    write_gbs = nbytes / t / 1e9
+    del buf, rsink, sink
+    return {"mfma_bf16_TFLOPs": mfma_tflops, "read_GBps": read_gbs, "write_GBps": write_gbs,
+            "copy_GBps": copy_gbs,
+            "note": "measured on this device: bf16 32x32x16 products on 8 independent "
+                    "accumulators per wave, 2 workgroups of 256 per CU; streaming 16-byte "
+                    "read of 1 GiB, torch fill of 1 GiB (write), copy of 512 MiB (read + "
+                    "write bytes).  A kernel's practical ceiling is its bytes over "
+                    "read_bytes / read_GBps + written_bytes / write_GBps"}
+
+
+def practical_frac(gbs, total_bytes, read_bytes, ceil):
+    """Achieved GB/s over the time-additive ceiling at the kernel's byte mix."""
+    w = total_bytes - read_bytes
+    t = read_bytes / ceil["read_GBps"] + w / ceil["write_GBps"]
+    return gbs / (total_bytes / t)
 
 
 def main():
@@ -288,6 +357,8 @@ def main():
     d_gbs = dev_bytes / (np.median(d_f) * 1e-3) / 1e9
     sd_gbs = sd_bytes / (np.median(sd_f) * 1e-3) / 1e9
 
+    log("[bench] practical ceilings")
+    ceil = measure_ceilings(torch)
     if args.calibrate_copy_mb:
         src = torch.ones(args.calibrate_copy_mb << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -330,7 +401,9 @@ def main():
             "flops_per_launch": attn_flops_launch, "ms_per_launch": attn_ms_launch,
             "ms_per_launch_p10_p50_p90": [attn_p10, attn_p50, attn_p90],
             "timing": "HIP events around each call in eager steps",
+            "frac_of_measured_ceiling": attn_tflops / ceil["mfma_bf16_TFLOPs"],
         },
+        "ceilings": ceil,
         "kernels": {
             "ms_per_step_eager": ms_step_eager, "ms_per_step_graph": ms_step_graph,
             ("stitch_deviation_ms" if fused else "stitch_ms"): float(st_ms),
@@ -348,6 +421,14 @@ def main():
             "chunk_importance_hbm_frac": imp_gbs / HBM_PEAK_GBS,
             "chunk_importance_bytes": int(imp_bytes),
             "selected_rows_per_layer": float(np.mean(cu[:, -1])),
+            "stitch_frac_of_practical": practical_frac(st_gbs, st_bytes,
+                                                       algorithmic.reads["stitch"], ceil),
+            "deviation_frac_of_practical": practical_frac(d_gbs, dev_bytes,
+                                                          algorithmic.reads["deviation"], ceil),
+            "stitch_deviation_frac_of_practical": practical_frac(
+                sd_gbs, sd_bytes, algorithmic.reads["stitch_deviation"], ceil),
+            "chunk_importance_frac_of_practical": practical_frac(
+                imp_gbs, imp_bytes, imp_bytes - P * 8, ceil),
         },
     }
     if not args.no_cpu_baseline:

@@ -1,7 +1,9 @@
 """Build libkvb.so (HIP for gfx950) in-tree with hipcc.
 
 ``python -m paper_2608_21362_amd.build`` compiles every source under
-``csrc/`` and links ``lib/libkvb.so``.  Objects go to ``_build/``.
+``csrc/`` and links ``lib/libkvb.so``, then builds ``lib/libkvb_ceiling.so``
+(the practical-ceiling kernels the benchmark measures) from ``ceiling/``.
+Objects go to ``_build/``.
 """
 import concurrent.futures as cf
 import os
@@ -16,6 +18,9 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB_DIR = os.path.join(PKG, "lib")
 LIB = os.path.join(LIB_DIR, "libkvb.so")
+# practical-ceiling kernels the benchmark measures next to the path (not part of libkvb)
+CEILING_SRC = os.path.join(PKG, "ceiling", "ceiling.hip")
+CEILING_LIB = os.path.join(LIB_DIR, "libkvb_ceiling.so")
 ARCH = "gfx950"
 
 COMMON = [
@@ -57,6 +62,12 @@ def build(jobs: int = 8) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, LIB)
+    tmp = CEILING_LIB + ".tmp"
+    cmd = [hipcc(), *COMMON, "-shared", "-x", "hip", CEILING_SRC, "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, CEILING_LIB)
     return LIB
 
 

@@ -36,6 +36,23 @@ def test_every_declared_symbol_is_exported():
     assert kvb.kvb_abi_version() == 4
 
 
+def test_ceiling_library_loads():
+    """The benchmark's practical-ceiling kernels build into their own library
+    and export their three entry points (no compute call here)."""
+    import os
+
+    path = os.path.join(os.path.dirname(kvb.LIB_PATH), "libkvb_ceiling.so")
+    lib = ctypes.CDLL(path)
+    for n in ("kvb_ceiling_mfma", "kvb_ceiling_read", "kvb_ceiling_copy"):
+        assert hasattr(lib, n), n
+    # argument checks reject before any launch
+    lib.kvb_ceiling_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    assert lib.kvb_ceiling_mfma(0, 10, ctypes.c_void_p(FAKE), None) == -1
+    lib.kvb_ceiling_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                     ctypes.c_void_p, ctypes.c_void_p]
+    assert lib.kvb_ceiling_read(ctypes.c_void_p(FAKE), 24, 8, ctypes.c_void_p(FAKE), None) == -1
+
+
 @pytest.mark.parametrize("theta,d", [(1e4, 64), (1e6, 128)])
 def test_rope_table_matches_oracle_bitwise(theta, d):
     delta = np.array([0, 1, -1, 1000, -32767, 32767, 12345, -5], np.int32)
