@@ -17,8 +17,9 @@
  *                       GQA attention of the selected query rows (Eq. 2)
  *
  * plus the host helpers that prepare their inputs (rotation tables, row
- * flags) and the cache-population kernels (RoPE at absolute positions, KIVI
- * quantisation, chunk importance; Sec. 4.6 warm, Sec. 4.4).
+ * flags, the threshold-activated probe of Sec. 7.4) and the cache-population
+ * kernels (RoPE at absolute positions, KIVI quantisation, chunk importance;
+ * Sec. 4.6 warm, Sec. 4.4).
  *
  * Conventions
  *   - Every pointer named as a tensor, descriptor, index or workspace is a
