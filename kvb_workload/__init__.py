@@ -75,9 +75,10 @@ class Workload:
         return self.n_q_heads // self.n_kv_heads
 
 
-# The five workloads.  Readings of unstated details (group sizes, seeds of the
-# second and fourth workload, hit placement of the batched one) are listed in
-# DESIGN.md under "Readings".
+# The five workloads.  Some details are choices made here, not given by the
+# paper: the statistic group sizes, the seeds of the second and fourth
+# workload, and the batched workload's hit placement (half of each prompt's
+# chunks, cached at multiples of 128).
 WORKLOADS: Dict[str, Workload] = {
     "tiny": Workload(
         name="tiny", n_layers=1, n_q_heads=4, n_kv_heads=2, head_dim=64,
