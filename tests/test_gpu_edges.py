@@ -1,0 +1,118 @@
+"""Edge cases of the selection and the attention through the C ABI, on
+generator-drawn inputs: ragged batches with empty prompts, one-row prompts and
+prompts with no selected row, both head sizes, with and without the fp16 shadow
+of V.  Selection bit-exact with the oracle; patch bit-exact; attention within
+|o - o_ref| <= 2e-2 + 1e-2 |o_ref|; rows that are not selected never written."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as oatt
+from oracle import numerics, selection as osel
+
+pytestmark = pytest.mark.gpu
+ATOL, RTOL = 2e-2, 1e-2
+LENS = [0, 37, 0, 129, 1, 640, 0, 255, 3]
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _bf16(rng, shape, scale=1.0):
+    return numerics.f32_to_bf16_bits((rng.standard_normal(shape) * scale).astype(np.float32))
+
+
+def test_select_empty_and_tiny_prompts():
+    _need_gpu()
+    from paper_2608_21362_amd import kvb
+
+    rng = np.random.default_rng(3)
+    cu = np.concatenate([[0], np.cumsum(LENS)]).astype(np.int32)
+    T, B, n_sets = int(cu[-1]), len(LENS), 2
+    cand = rng.random(T) < 0.7
+    forced = (~cand) | (rng.random(T) < 0.03)
+    flags = (cand.astype(np.uint8) * kvb.KVB_ROW_CANDIDATE) | (forced.astype(np.uint8) * kvb.KVB_ROW_FORCED)
+    delta = rng.random((n_sets, T)).astype(np.float32)
+    ks = np.stack([osel.k_per_prompt(cu, cand, 15, 100), osel.k_per_prompt(cu, cand, 60, 100)])
+    ks = ks.astype(np.int32)
+    ws_bytes = kvb.kvb_select_workspace_bytes(n_sets, T, B)
+    d_rows = torch.full((n_sets, T), -1, dtype=torch.int32, device="cuda")
+    d_cur = torch.zeros((n_sets, B + 1), dtype=torch.int32, device="cuda")
+    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device="cuda")
+    kvb.kvb_select(n_sets, T, torch.from_numpy(cu).cuda(), B, torch.from_numpy(delta).cuda(),
+                   torch.from_numpy(flags).cuda(), torch.from_numpy(ks).cuda(), d_rows, d_cur, ws,
+                   ws_bytes)
+    torch.cuda.synchronize()
+    g_rows, g_cu = d_rows.cpu().numpy(), d_cur.cpu().numpy()
+    for si in range(n_sets):
+        r_rows, r_cu = osel.select(delta[si], cand, forced, cu, ks[si])
+        assert np.array_equal(g_cu[si], r_cu), si
+        assert np.array_equal(g_rows[si, : r_cu[-1]], r_rows), si
+        # empty prompts own no rows of the list
+        for b in np.flatnonzero(np.diff(cu) == 0):
+            assert g_cu[si, b] == g_cu[si, b + 1]
+
+
+@pytest.mark.parametrize("hq,hkv,d,shadow", [(16, 2, 128, True), (16, 2, 128, False),
+                                            (4, 2, 64, True), (8, 8, 64, False)])
+def test_attention_ragged_with_empty_prompts(hq, hkv, d, shadow):
+    _need_gpu()
+    from paper_2608_21362_amd import kvb
+
+    _say(f"[edges] attention Hq={hq} Hkv={hkv} d={d} shadow={shadow}")
+    rng = np.random.default_rng(hq * 100 + d + shadow)
+    cu = np.concatenate([[0], np.cumsum(LENS)]).astype(np.int32)
+    T, B = int(cu[-1]), len(LENS)
+    q = _bf16(rng, (T, hq, d))
+    kc, vc = _bf16(rng, (hkv, T, d)), _bf16(rng, (hkv, T, d), 2.0)
+    kf, vf = _bf16(rng, (hkv, T, d)), _bf16(rng, (hkv, T, d), 2.0)
+    # selected rows: about a third of each prompt, none of the 129-row prompt,
+    # the one-row prompt's row, the whole 3-row prompt
+    rows = []
+    for b in range(B):
+        lo, hi = int(cu[b]), int(cu[b + 1])
+        if hi - lo in (0, 129):
+            continue
+        if hi - lo <= 3:
+            rows.extend(range(lo, hi))
+        else:
+            rows.extend(sorted(rng.choice(np.arange(lo, hi), size=(hi - lo) // 3, replace=False)))
+    rows = np.asarray(rows, dtype=np.int32)
+    cu_rows = np.searchsorted(rows, cu).astype(np.int32)
+    max_seq = int(np.max(np.diff(cu)))
+    dk, dv = torch.from_numpy(kc.view(np.int16)).cuda(), torch.from_numpy(vc.view(np.int16)).cuda()
+    v16 = None
+    if shadow:
+        v16 = torch.from_numpy(numerics.bf16_bits_to_f32(vc).astype(np.float16).view(np.int16)).cuda()
+    out = torch.full((T, hq, d), -1, dtype=torch.int16, device="cuda")
+    wsb = kvb.kvb_sparse_attn_workspace_bytes(1, hq, hkv, d, T, B, max_seq, len(rows), int(shadow))
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+    kvb.kvb_sparse_attn(1, hq, hkv, d, T, torch.from_numpy(cu).cuda(), B, max_seq,
+                        torch.from_numpy(rows).cuda(), torch.from_numpy(cu_rows).cuda(), 0,
+                        len(rows), torch.from_numpy(q.view(np.int16)).cuda(),
+                        torch.from_numpy(kf.view(np.int16)).cuda(),
+                        torch.from_numpy(vf.view(np.int16)).cuda(), dk, dv, v16,
+                        1.0 / np.sqrt(d), kvb.KVB_BF16, out, ws, wsb)
+    torch.cuda.synchronize()
+    pk, pv = oatt.patch(kc, kf, rows), oatt.patch(vc, vf, rows)
+    assert np.array_equal(dk.cpu().numpy().view(np.uint16), pk)
+    assert np.array_equal(dv.cpu().numpy().view(np.uint16), pv)
+    if shadow:
+        assert np.array_equal(v16.cpu().numpy().view(np.uint16),
+                              numerics.bf16_bits_to_f32(pv).astype(np.float16).view(np.uint16))
+    ref = oatt.attend_rows(q, pk, pv, rows, cu)
+    o = out.cpu().numpy().view(np.uint16)
+    got = numerics.bf16_bits_to_f32(o[rows]).astype(np.float64)
+    err = np.abs(got - ref)
+    _say(f"[edges] rows {len(rows)} max|err| {err.max():.3e}")
+    assert np.all(err <= ATOL + RTOL * np.abs(ref))
+    others = np.setdiff1d(np.arange(T), rows)
+    assert np.all(o[others] == 0xFFFF), "a row that was not selected was written"
