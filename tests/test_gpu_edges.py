@@ -1,7 +1,9 @@
-"""Edge cases of the selection and the attention through the C ABI, on
-generator-drawn inputs: ragged batches with empty prompts, one-row prompts and
-prompts with no selected row, both head sizes, with and without the fp16 shadow
-of V.  Selection bit-exact with the oracle; patch bit-exact; attention within
+"""Edge cases of the deviation, the selection and the attention through the C
+ABI, on generator-drawn inputs: zero and negative-zero vectors, identical rows,
+values in the deviation, all-layer deviation; ragged batches with empty
+prompts, one-row prompts and prompts with no selected row, both head sizes,
+with and without the fp16 shadow of V.  Deviation within one float32 ulp of
+the oracle; selection bit-exact; patch bit-exact; attention within
 |o - o_ref| <= 2e-2 + 1e-2 |o_ref|; rows that are not selected never written."""
 import sys
 
@@ -10,6 +12,7 @@ import pytest
 import torch
 
 from oracle import attention as oatt
+from oracle import deviation as odev
 from oracle import numerics, selection as osel
 
 pytestmark = pytest.mark.gpu
@@ -116,3 +119,41 @@ def test_attention_ragged_with_empty_prompts(hq, hkv, d, shadow):
     assert np.all(err <= ATOL + RTOL * np.abs(ref))
     others = np.setdiff1d(np.arange(T), rows)
     assert np.all(o[others] == 0xFFFF), "a row that was not selected was written"
+
+
+@pytest.mark.parametrize("with_v,per_layer,d", [(False, True, 128), (True, True, 128),
+                                                (True, False, 64), (False, False, 128)])
+def test_deviation_zero_rows_and_values(with_v, per_layer, d):
+    """kvb_deviation alone: planted rows where both vectors are zero (cosine 1),
+    one of them is zero (cosine 0), -0 entries, identical rows (delta 0 exactly
+    per term), with the values entering or not, per layer or over all layers:
+    within one float32 ulp of the oracle."""
+    _need_gpu()
+    from paper_2608_21362_amd import kvb
+
+    rng = np.random.default_rng(d + 2 * with_v + per_layer)
+    L, H, T = 3, 2, 700
+    kc, kf = _bf16(rng, (L, H, T, d)), _bf16(rng, (L, H, T, d))
+    vc, vf = _bf16(rng, (L, H, T, d), 3.0), _bf16(rng, (L, H, T, d), 3.0)
+    kf[:, :, 10:20] = kc[:, :, 10:20]           # identical rows
+    kc[:, :, 30:35] = 0                          # both zero
+    kf[:, :, 30:35] = 0
+    kc[:, :, 40:45] = 0                          # cache zero only
+    kf[:, :, 50:55] = 0x8000                     # fresh -0 only
+    kc[1, 0, 60] = 0                             # a zero in one layer and head only
+    vc[:, :, 70:72] = 0
+    vf[:, :, 70:72] = 0
+    n_sets = L if per_layer else 1
+    delta = torch.full((n_sets, T), -5.0, dtype=torch.float32, device="cuda")
+    t = lambda a: torch.from_numpy(a.view(np.int16)).cuda()  # noqa: E731
+    kvb.kvb_deviation(L, H, d, T, t(kc), t(kf), t(vc) if with_v else None,
+                      t(vf) if with_v else None, int(per_layer), delta)
+    torch.cuda.synchronize()
+    ref = odev.deviation(kc, kf, vc if with_v else None, vf if with_v else None,
+                         per_layer=per_layer).astype(np.float32)
+    got = delta.cpu().numpy()
+    ulp = np.spacing(np.abs(ref))
+    assert np.all(np.abs(got.astype(np.float64) - ref) <= ulp)
+    if not with_v:
+        assert np.all(got[:, 10:20] == 0.0) and np.all(got[:, 30:35] == 0.0)
+        assert np.all(got[:, 40:45] == 1.0) and np.all(got[:, 50:55] == 1.0)
