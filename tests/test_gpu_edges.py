@@ -1,5 +1,5 @@
-"""Edge cases of the deviation, the selection and the attention through the C
-ABI, on generator-drawn inputs: zero and negative-zero vectors, identical rows,
+"""Edge cases of the stitch, the deviation, the selection and the attention
+through the C ABI, on generator-drawn inputs: out-of-range chunk descriptors; zero and negative-zero vectors, identical rows,
 values in the deviation, all-layer deviation; ragged batches with empty
 prompts, one-row prompts and prompts with no selected row, both head sizes,
 with and without the fp16 shadow of V.  Deviation within one float32 ulp of
@@ -157,3 +157,40 @@ def test_deviation_zero_rows_and_values(with_v, per_layer, d):
     if not with_v:
         assert np.all(got[:, 10:20] == 0.0) and np.all(got[:, 30:35] == 0.0)
         assert np.all(got[:, 40:45] == 1.0) and np.all(got[:, 50:55] == 1.0)
+
+
+def test_stitch_skips_out_of_range_descriptors():
+    """Descriptors whose pool slot or destination rows fall outside the arrays
+    are skipped (nothing written); the valid ones in the same list are stitched
+    bit-exact with the oracle."""
+    _need_gpu()
+    import kvb_workload as kw
+    from oracle import populate as opop, stitch as ostitch
+    from paper_2608_21362_amd import kvb, pipeline
+
+    # half of the chunks are misses: the bad descriptors point at live rows,
+    # which no valid descriptor writes, so a write there would show
+    w = kw.scaled(kw.WORKLOADS["batched_mixed"], n_prompts=2, chunks_per_prompt=4)
+    s = kw.structure(w)
+    dev = pipeline.populate(w, s)
+    ref = opop.populate(w, s)
+    P, T = s.n_pool, w.t_total
+    good = ref.chunks.copy()
+    live = [r for r in range(0, T, 128) if not s.hit_row[r]]
+    assert len(live) >= 2
+    bad = np.array([[P, 0, live[0], 0], [-1, 0, live[1], 128], [0, 0, T - 64, 0],
+                    [1, 0, -128, 0]], dtype=np.int32)
+    chunks = np.concatenate([bad[:2], good, bad[2:]])
+    cos = np.concatenate([ref.cos[:2] * 0, ref.cos, ref.cos[:2] * 0]).astype(np.float32)
+    sin = np.concatenate([ref.sin[:2] * 0, ref.sin, ref.sin[:2] * 0]).astype(np.float32)
+    pb = pipeline.buffers(dev)
+    kvb.kvb_stitch(dev.pool, P, dev.k_codes, dev.k_scale, dev.k_zero, dev.v_codes, dev.v_scale,
+                   dev.v_zero, torch.from_numpy(chunks).cuda(), len(chunks),
+                   torch.from_numpy(np.ascontiguousarray(cos)).cuda(),
+                   torch.from_numpy(np.ascontiguousarray(sin)).cuda(), T, kvb.KVB_BF16,
+                   pb.k_cache, pb.v_cache, None)
+    torch.cuda.synchronize()
+    ck, cv = ref.cache_k.copy(), ref.cache_v.copy()
+    ostitch.stitch_into(ck, cv, ref.pool, ref.chunks, ref.cos, ref.sin, "bf16")
+    assert np.array_equal(pb.k_cache.cpu().numpy().view(np.uint16), ck)
+    assert np.array_equal(pb.v_cache.cpu().numpy().view(np.uint16), cv)
