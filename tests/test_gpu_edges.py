@@ -1,9 +1,10 @@
 """Edge cases of the stitch, the deviation, the selection and the attention
-through the C ABI, on generator-drawn inputs: out-of-range chunk descriptors; zero and negative-zero vectors, identical rows,
-values in the deviation, all-layer deviation; ragged batches with empty
-prompts, one-row prompts and prompts with no selected row, both head sizes,
-with and without the fp16 shadow of V.  Deviation within one float32 ulp of
-the oracle; selection bit-exact; patch bit-exact; attention within
+through the C ABI, on generator-drawn inputs: out-of-range chunk descriptors;
+zero and negative-zero vectors, identical rows, values in the deviation,
+all-layer deviation; ragged batches with empty prompts, one-row prompts and
+prompts with no selected row, both head sizes, with and without the fp16
+shadow of V.  Stitch bit-exact; deviation within one float32 ulp of the
+oracle; selection bit-exact; patch bit-exact; attention within
 |o - o_ref| <= 2e-2 + 1e-2 |o_ref|; rows that are not selected never written."""
 import sys
 
