@@ -572,35 +572,47 @@ __device__ __forceinline__ void attend_segment(
   }
 }
 
-// Plan area (int32): [0] c1, [1] c2, [2] n_first, [3] total, [4 .. 4+n_tiles]
-// prefix, [5+n_tiles ..) first tile of every workgroup, then the per-tile
-// metadata (int4) at this offset.
+// Plan area (int32): [0] c1, [1] c2, [2] n_second, [3] total, [4 .. 4+n_tiles]
+// prefix, [5+n_tiles ..) first tile of every workgroup (by range index), then
+// the per-tile metadata (int4) at this offset.
 __host__ __device__ constexpr int64_t tile_meta_offset(int64_t n_tiles, int64_t n_wg_max) {
   return ((5 + n_tiles + n_wg_max + 3) / 4) * 4;
 }
 
-// First unit of workgroup w: the first n_first workgroups take c1 units each,
-// the others c2.
-__device__ __forceinline__ int unit_start(int w, int c1, int c2, int nf) {
-  return w < nf ? w * c1 : nf * c1 + (w - nf) * c2;
+// Ranges are numbered by a range index v: the n2 second-slot workgroups take
+// ranges 0 .. n2-1 (c2 units each), the first-slot ones the ranges after them
+// (c1 units each).  Tiles are ordered shortest first (below), so the tiles
+// with the fewest blocks -- the workgroups that cover several of them pay a
+// segment's fixed cost several times -- go to second-slot workgroups, for which
+// the segment cost in units (kSegCost) is closest to its time.
+__device__ __forceinline__ int unit_start(int v, int c1, int c2, int n2) {
+  return v < n2 ? v * c2 : n2 * c2 + (v - n2) * c1;
 }
 
-// Workgroup whose range holds unit u.
-__device__ __forceinline__ int unit_owner(int u, int c1, int c2, int nf) {
-  const int b = nf * c1;
-  return u < b ? u / c1 : nf + (u - b) / c2;
+// Range index whose units hold unit u.
+__device__ __forceinline__ int unit_owner(int u, int c1, int c2, int n2) {
+  const int b = n2 * c2;
+  return u < b ? u / c2 : n2 + (u - b) / c1;
+}
+
+// Range index of workgroup w (workgroups 0 .. n_first-1 take the first slot of
+// each CU).
+__device__ __forceinline__ int range_of(int w, int n_first, int n2) {
+  return w >= n_first ? w - n_first : n2 + w;
 }
 
 // Work decomposition.  Work unit = one 32-key block of one tile, and a tile
 // with blocks also counts kSegCost units for its fixed cost (they come first
-// and hold no blocks); units are numbered tile by tile (tile index =
-// (layer x kv head) * tile_slots + slot).  One workgroup builds the exclusive
-// prefix sum of the tiles' unit counts, then attention workgroup w takes the
-// contiguous units [unit_start(w), unit_start(w + 1)): c1 units for each of the
-// first n_first workgroups, c2 for the others, sized to cover every unit.
-//   plan[0] = c1, plan[1] = c2, plan[2] = n_first, plan[3] = total,
+// and hold no blocks); units are numbered tile by tile, tiles slot-major (tile
+// index = slot * (layers x kv heads) + layer x kv head: the first row tiles of
+// every prompt, which attend to the fewest keys, come first).  One workgroup
+// builds the exclusive prefix sum of the tiles' unit counts, then the
+// attention workgroup with range index v takes the contiguous units
+// [unit_start(v), unit_start(v + 1)): c2 units for each of the first n2
+// ranges (second-slot workgroups), c1 for the others, sized to cover every unit.
+//   plan[0] = c1, plan[1] = c2, plan[2] = n2, plan[3] = total,
 //   plan[4 .. 4+n_tiles] = prefix,
-//   plan[5+n_tiles .. 5+n_tiles+n_wg) = tile holding unit unit_start(w),
+//   plan[5+n_tiles .. 5+n_tiles+n_wg) = tile holding unit unit_start(v),
 //   then per tile an int4 {first row entry, end row entry, key start, key end}
 //   at the 16-byte aligned offset tile_meta_offset(n_tiles, n_wg_max).
 __device__ __forceinline__ void build_plan(
@@ -622,7 +634,8 @@ __device__ __forceinline__ void build_plan(
     const int t = base + tid;
     int nb = 0;
     if (t < n_tiles) {
-      const int lg = t / tile_slots, slot = t % tile_slots;
+      const int n_lg = n_tiles / tile_slots;
+      const int lg = t % n_lg, slot = t / n_lg;
       const int64_t set = rows_per_layer ? lg / Hkv : 0;
       const int32_t* cur = cu_rows + set * (n_seqs + 1);
       Tile tile;
@@ -659,29 +672,30 @@ __device__ __forceinline__ void build_plan(
   const int64_t weight = (int64_t)kFirstShareNum * n_first + (int64_t)kFirstShareDen * (n_wg - n_first);
   const int c2 = (int)max((int64_t)1, ((int64_t)kFirstShareDen * total + weight - 1) / weight);
   const int c1 = (int)(((int64_t)kFirstShareNum * c2 + kFirstShareDen - 1) / kFirstShareDen);
+  const int n2 = n_wg - n_first;
   if (tid == 0) {
     plan[0] = c1;
     plan[1] = c2;
-    plan[2] = n_first;
+    plan[2] = n2;
     plan[3] = total;
     prefix[n_tiles] = total;
     prefix_sh[n_tiles] = total;
   }
   __syncthreads();
-  // tile holding unit unit_start(w): every non-empty tile [p0, p1) writes the
-  // workgroups whose first unit lies in it (one pass, no search); workgroups
-  // that start past the last unit get n_tiles (they have no work)
+  // tile holding unit unit_start(v): every non-empty tile [p0, p1) writes the
+  // ranges whose first unit lies in it (one pass, no search); ranges that
+  // start past the last unit get n_tiles (they have no work)
   for (int t = tid; t < n_tiles; t += nt) {
     const int p0 = prefix_sh[t], p1 = prefix_sh[t + 1];
     if (p1 <= p0) continue;
-    for (int w = unit_owner(p0, c1, c2, n_first); w < n_wg; ++w) {
-      const int u = unit_start(w, c1, c2, n_first);
+    for (int v = unit_owner(p0, c1, c2, n2); v < n_wg; ++v) {
+      const int u = unit_start(v, c1, c2, n2);
       if (u >= p1) break;
-      if (u >= p0) first[w] = t;
+      if (u >= p0) first[v] = t;
     }
   }
-  for (int w = tid; w < n_wg; w += nt)
-    if (unit_start(w, c1, c2, n_first) >= total) first[w] = n_tiles;
+  for (int v = tid; v < n_wg; v += nt)
+    if (unit_start(v, c1, c2, n2) >= total) first[v] = n_tiles;
 }
 
 // Patch: cache[l][h][t] <- fresh[l][h][t] for every selected row t (both
@@ -754,10 +768,11 @@ attn_kernel(int32_t balanced, int32_t n_tiles, int32_t Hq, int32_t Hkv, int32_t 
   __shared__ __attribute__((aligned(1024))) char v_ring[kStages * C::BLK];
   if (!balanced) {
     const int t = blockIdx.x;
-    const int lg = t / tile_slots;
+    const int n_lg = n_tiles / tile_slots;
+    const int lg = t % n_lg;
     const int64_t set = rows_per_layer ? lg / Hkv : 0;
     Tile tile;
-    if (!find_tile(cu_rows + set * (n_seqs + 1), n_seqs, rows_per_tile, t % tile_slots, &tile))
+    if (!find_tile(cu_rows + set * (n_seqs + 1), n_seqs, rows_per_tile, t / n_lg, &tile))
       return;
     SegTile tl;
     tl.lg = lg;
@@ -770,13 +785,14 @@ attn_kernel(int32_t balanced, int32_t n_tiles, int32_t Hq, int32_t Hkv, int32_t 
                       rows_per_layer, q, kc, v16, c_log2, out_f32, out, parts);
     return;
   }
-  const int w = blockIdx.x;
-  const int c1 = plan[0], c2 = plan[1], nf = plan[2], total = plan[3];
+  const int c1 = plan[0], c2 = plan[1], n2 = plan[2], total = plan[3];
+  const int n_lg = n_tiles / tile_slots;
+  const int v = range_of(blockIdx.x, (int)gridDim.x - n2, n2);  // range index
   const int32_t* prefix = plan + 4;
   const int4* meta = reinterpret_cast<const int4*>(plan + tile_meta_offset(n_tiles, n_wg_max));
-  int u = unit_start(w, c1, c2, nf);
-  const int u_end = min(unit_start(w + 1, c1, c2, nf), total);
-  int t = plan[5 + n_tiles + w];
+  int u = unit_start(v, c1, c2, n2);
+  const int u_end = min(unit_start(v + 1, c1, c2, n2), total);
+  int t = plan[5 + n_tiles + v];
   for (int seg = 0; u < u_end && t < n_tiles; ++t) {
     const int p0 = prefix[t], p1 = prefix[t + 1];
     if (p1 <= u) continue;  // empty tile (or before the range)
@@ -784,10 +800,10 @@ attn_kernel(int32_t balanced, int32_t n_tiles, int32_t Hq, int32_t Hkv, int32_t 
     // units [p0, p0 + kSegCost) of a tile stand for its fixed cost and hold no block
     const int b_lo = max(u - p0 - kSegCost, 0), b_hi = max(e - p0 - kSegCost, 0);
     if (b_hi > b_lo) {
-      const int rec = (u <= p0 + kSegCost && p1 <= u_end) ? -1 : 2 * w + (seg == 0 ? 0 : 1);
+      const int rec = (u <= p0 + kSegCost && p1 <= u_end) ? -1 : 2 * v + (seg == 0 ? 0 : 1);
       const int4 mt = meta[t];
       SegTile tl;
-      tl.lg = t / tile_slots;
+      tl.lg = t % n_lg;
       tl.r_begin = mt.x;
       tl.r_end = mt.y;
       tl.kstart = mt.z;
@@ -811,28 +827,28 @@ combine_kernel(int32_t n_tiles, int32_t n_wg_max, int32_t Hq, int32_t Hkv, int32
                int32_t tile_slots, const int32_t* __restrict__ plan, int32_t n_rec,
                int32_t out_f32, void* __restrict__ out, const float* __restrict__ parts) {
   const int t = blockIdx.x;
-  const int c1 = plan[0], c2 = plan[1], nf = plan[2];
+  const int c1 = plan[0], c2 = plan[1], n2 = plan[2];
   const int p0 = plan[4 + t], p1 = plan[5 + t];
   const int4 mt = reinterpret_cast<const int4*>(plan + tile_meta_offset(n_tiles, n_wg_max))[t];
   if (p1 <= p0) return;
-  // the tile's blocks are units [p0 + kSegCost, p1)
-  const int w_a = unit_owner(p0 + kSegCost, c1, c2, nf), w_b = unit_owner(p1 - 1, c1, c2, nf);
+  // the tile's blocks are units [p0 + kSegCost, p1), held by ranges w_a .. w_b
+  const int w_a = unit_owner(p0 + kSegCost, c1, c2, n2), w_b = unit_owner(p1 - 1, c1, c2, n2);
   if (w_a == w_b) return;  // finished by one workgroup
   constexpr int Q8 = D / 8;  // 8-channel pieces per query vector
   const int e = blockIdx.y * blockDim.x + threadIdx.x;
   if (e >= kQT * Q8) return;
   const int qi = e / Q8, c8 = (e % Q8) * 8;
-  const int lg = t / tile_slots;
+  const int lg = t % (n_tiles / tile_slots);
   const int l = lg / Hkv, g = lg % Hkv;
   const int wave = qi / kQW, nq = qi % kQW;
   const int row_idx = mt.x + wave * (kQW >> log2g) + (nq >> log2g);
   if (row_idx >= mt.y) return;
   const int64_t set = rows_per_layer ? l : 0;
   const int tq = rows[set * t_total + row_idx];
-  // the tile is the first segment of every workgroup after w_a, and of w_a
-  // only if w_a's range starts inside the tile (a range that starts before it
-  // ends with blocks of an earlier tile)
-  const int rec_a = 2 * w_a + (unit_start(w_a, c1, c2, nf) < p0 ? 1 : 0);
+  // the tile is the first segment of every range after w_a, and of w_a only
+  // if w_a's range starts inside the tile (a range that starts before it ends
+  // with blocks of an earlier tile)
+  const int rec_a = 2 * w_a + (unit_start(w_a, c1, c2, n2) < p0 ? 1 : 0);
   const int n_parts = w_b - w_a + 1;
   const uint16_t* o16 = reinterpret_cast<const uint16_t*>(parts);
   const float* ml = reinterpret_cast<const float*>(reinterpret_cast<const char*>(parts) +
