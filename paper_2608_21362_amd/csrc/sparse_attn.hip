@@ -767,7 +767,9 @@ attn_kernel(int32_t balanced, int32_t n_tiles, int32_t Hq, int32_t Hkv, int32_t 
   __shared__ __attribute__((aligned(1024))) char k_ring[kStages * C::BLK];
   __shared__ __attribute__((aligned(1024))) char v_ring[kStages * C::BLK];
   if (!balanced) {
-    const int t = blockIdx.x;
+    // tiles in reverse order: the last row tiles of a prompt, which attend to
+    // the most keys, are dispatched first and the launch ends on short ones
+    const int t = n_tiles - 1 - (int)blockIdx.x;
     const int n_lg = n_tiles / tile_slots;
     const int lg = t % n_lg;
     const int64_t set = rows_per_layer ? lg / Hkv : 0;
