@@ -70,19 +70,24 @@ def algorithmic(w, s, rows_per_set, cu_rows_per_set):
     return stitch_bytes, dev_bytes, fused_bytes, np.array(flops_per_layer)
 
 
-def committed_traffic(workload):
+def committed_traffic(workload, key="traffic_bytes_per_launch"):
     """Per-launch HBM bytes of the attention call from the committed counter
-    summary, if it was taken on the current kernel sources (else None)."""
+    summary, if it was taken on the current kernel sources (else None).  The
+    summary's ``traffic_bytes_per_launch`` covers attention + combine (one
+    kvb_sparse_attn_layer call), ``traffic_bytes_per_launch_with_patch`` adds
+    the patch (one per-layer kvb_sparse_attn call)."""
     import hashlib
     import re
     path = os.path.join(ROOT, "profiles", f"sparse_attn_{workload}_traffic.md")
     if not os.path.exists(path):
         return None, "no committed counter summary"
     text = open(path).read()
-    m_b = re.search(r"^traffic_bytes_per_launch:\s*([0-9.eE+]+)", text, re.M)
+    m_b = re.search(r"^" + key + r":\s*([0-9.eE+]+)", text, re.M)
     m_h = re.search(r"^kernel_sources_sha256:\s*([0-9a-f]+)", text, re.M)
-    if not (m_b and m_h):
-        return None, "summary lacks the traffic or source-hash line"
+    if not m_h:
+        return None, "summary lacks the source-hash line"
+    if not m_b:
+        return None, f"summary holds no {key} figure (no counters for this call grouping)"
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
         h.update(open(os.path.join(ROOT, f), "rb").read())
@@ -193,6 +198,9 @@ def main():
     ap.add_argument("--workload", default="qwen_36l_8k")
     ap.add_argument("--attn-all-layers", action="store_true",
                     help="one attention launch for all layers (ceiling variant)")
+    ap.add_argument("--patch-per-layer", action="store_true",
+                    help="patch inside every per-layer kvb_sparse_attn call instead of one "
+                         "kvb_patch of every layer before the per-layer calls")
     ap.add_argument("--unfused", action="store_true",
                     help="separate stitch and deviation + selection calls instead of the fused "
                          "stitch + deviation call followed by selection")
@@ -231,6 +239,8 @@ def main():
     L = di.n_layers
 
     fused = not args.unfused
+    patch_once = not args.patch_per_layer and not args.attn_all_layers
+    a0 = 4 if patch_once else 3  # event index after which the attention calls start
 
     def step(rec=None):
         if rec is not None:
@@ -251,6 +261,16 @@ def main():
             pipeline.sparse_attn_all(di, pb)
             if rec is not None:
                 rec[3].record(stream)
+        elif patch_once:
+            # Alg. 2 step 4 for every layer, then the repair forward's
+            # attention layer by layer
+            pipeline.patch(di, pb)
+            if rec is not None:
+                rec[3].record(stream)
+            for i in range(L):
+                pipeline.attn_layer(di, pb, i)
+                if rec is not None:
+                    rec[4 + i].record(stream)
         else:
             for i in range(L):
                 pipeline.sparse_attn_layer(di, pb, i)
@@ -287,7 +307,7 @@ def main():
 
     # Eager steps with HIP events around every call: per-kernel times and the
     # attention call's duration for the roofline
-    n_ev = 3 + (1 if args.attn_all_layers else L)
+    n_ev = a0 + (1 if args.attn_all_layers else L)
     recs = [[ev() for _ in range(n_ev)] for _ in range(args.steps)]
     start, stop = ev(), ev()
     torch.cuda.synchronize()
@@ -301,7 +321,9 @@ def main():
     ms_step = ms_step_graph if graph_same else ms_step_eager
     st_ms = np.mean([r[0].elapsed_time(r[1]) for r in recs])
     dv_ms = np.mean([r[1].elapsed_time(r[2]) for r in recs])
-    at_ms = np.array([[r[2 + j].elapsed_time(r[3 + j]) for j in range(n_ev - 3)] for r in recs])
+    pt_ms = float(np.mean([r[2].elapsed_time(r[3]) for r in recs])) if patch_once else None
+    at_ms = np.array([[r[a0 - 1 + j].elapsed_time(r[a0 + j]) for j in range(n_ev - a0)]
+                      for r in recs])
     attn_ms_launch = float(at_ms.mean())
     attn_p10, attn_p50, attn_p90 = (float(np.percentile(at_ms, p)) for p in (10, 50, 90))
 
@@ -367,7 +389,10 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    traffic, traffic_note = committed_traffic(w.name) if not args.attn_all_layers else (None, "")
+    traffic, traffic_note = (
+        (None, "") if args.attn_all_layers else
+        committed_traffic(w.name, "traffic_bytes_per_launch" if patch_once
+                          else "traffic_bytes_per_launch_with_patch"))
     tokens_per_step = w.t_total
     result = {
         "metric": METRIC,
@@ -387,14 +412,20 @@ def main():
             "q_heads": w.n_q_heads, "kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
             "kivi_bits": w.bits, "k_group": w.k_group, "v_group": w.v_group,
             "cached_chunks": s.n_pool, "recompute": f"{w.rho_num}/{w.rho_den} per layer",
-            "attention_launches": "one per layer" if not args.attn_all_layers else "one for all layers",
+            "attention_launches": ("one patch of every layer, then one call per layer" if patch_once
+                                   else "patch and attention per layer" if not args.attn_all_layers
+                                   else "one for all layers"),
             "stitch_and_deviation": "fused (kvb_stitch_deviation, then kvb_select)" if fused
             else "separate (kvb_stitch, then kvb_deviation_topk)",
             "step_timing": "HIP graph replay" if graph_same else "eager (graph replay differed)",
             "parallelism": "single GPU",
         },
         "roofline": {
-            "kernel": "kvb_sparse_attn call per layer (patch, attention and combine kernels)",
+            "kernel": ("kvb_sparse_attn_layer call per layer (attention and combine kernels)"
+                       if patch_once else
+                       "kvb_sparse_attn call per layer (patch, attention and combine kernels)"
+                       if not args.attn_all_layers else
+                       "kvb_sparse_attn call for all layers (patch, attention and combine kernels)"),
             "bound": "mfma", "achieved": attn_tflops, "peak": MFMA_BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s", "frac": attn_tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": traffic,
             "traffic_note": traffic_note,
@@ -408,6 +439,7 @@ def main():
             "ms_per_step_eager": ms_step_eager, "ms_per_step_graph": ms_step_graph,
             ("stitch_deviation_ms" if fused else "stitch_ms"): float(st_ms),
             ("select_ms" if fused else "deviation_topk_ms"): float(dv_ms),
+            "patch_ms": pt_ms,
             "sparse_attn_ms_per_step": float(at_ms.sum(axis=1).mean()),
             "stitch_GBps_flushed": st_gbs, "stitch_hbm_frac": st_gbs / HBM_PEAK_GBS,
             "stitch_bytes": st_bytes,

@@ -15,6 +15,10 @@
  *   kvb_deviation_topk  kvb_deviation followed by kvb_select
  *   kvb_sparse_attn     patch the selected rows (Alg. 2 step 4), then causal
  *                       GQA attention of the selected query rows (Eq. 2)
+ *   kvb_patch           Alg. 2 step 4 alone, every layer at once, and the
+ *                       attention work plans of every layer
+ *   kvb_sparse_attn_layer  the repair forward's attention of one layer over
+ *                       the patched cache (Eq. 2), with its prebuilt plan
  *
  * plus the host helpers that prepare their inputs (rotation tables, row
  * flags, the threshold-activated probe of Sec. 7.4) and the cache-population
@@ -86,10 +90,11 @@ typedef struct {
   int32_t pool_idx, src_pos, dst_row, dst_pos;
 } kvb_chunk;
 
-/* 4 for this header (version 2 added the optional fp16 shadow of V to
+/* 5 for this header (version 2 added the optional fp16 shadow of V to
  * kvb_stitch, kvb_sparse_attn and kvb_sparse_attn_workspace_bytes; version 3
  * added kvb_stitch_deviation and kvb_chunk_importance; version 4 added
- * kvb_probe_gate). */
+ * kvb_probe_gate; version 5 added kvb_attn_plans_bytes, kvb_patch and
+ * kvb_sparse_attn_layer). */
 int kvb_abi_version(void);
 
 /* Thread-local message of the last failing call on this thread. */
@@ -330,6 +335,62 @@ kvb_status kvb_sparse_attn(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_hea
                            uint16_t* k_cache, uint16_t* v_cache, uint16_t* v_cache_f16,
                            float softmax_scale, kvb_dtype out_dtype, void* out, void* workspace,
                            size_t workspace_bytes, void* stream);
+
+/* ---- patch once, then attention layer by layer -------------------------
+ * Alg. 2 takes the rows it patches (K~, V~) from the probe pass, which covers
+ * every layer before the selection (step 1), and step 4 completes before the
+ * repair forward runs.  A caller that runs the repair forward layer by layer
+ * can therefore patch every layer with one kvb_patch call right after the
+ * selection, then make one kvb_sparse_attn_layer call per layer.  Results
+ * (cache, fp16 shadow, out) are bit-identical to kvb_sparse_attn over the same
+ * rows. */
+
+/* Bytes of the plan buffer kvb_patch fills for n_layers layers (pure
+ * function; 0 for invalid sizes).  The plans depend on the sizes given here and
+ * on the device's compute-unit count: build and use them on one device. */
+size_t kvb_attn_plans_bytes(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads,
+                            int32_t head_dim, int64_t t_total, int32_t n_seqs,
+                            int32_t max_seq_len, int32_t max_rows);
+
+/* Patch (Alg. 2 step 4) of every layer: for each layer l and t in S_l (rows[l]
+ * / cu_rows[l] when rows_per_layer, else rows[0] / cu_rows[0]) and kv head h,
+ * k_cache[l][h][t] = k_fresh[l][h][t], v_cache[l][h][t] = v_fresh[l][h][t] and,
+ * when v_cache_f16 is given, v_cache_f16[l][h][t] = fp16 of v_fresh[l][h][t].
+ * Layouts and sizes as kvb_sparse_attn.  When plans is not NULL the same launch
+ * also writes the attention work plan of every layer into it (at least
+ * kvb_attn_plans_bytes bytes, 16-byte aligned; the contents are opaque), for
+ * the kvb_sparse_attn_layer calls that follow on the same rows.
+ * Errors: KVB_EINVAL (incl. plans smaller than kvb_attn_plans_bytes),
+ * KVB_EUNSUPPORTED (as kvb_sparse_attn). */
+kvb_status kvb_patch(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                     int64_t t_total, const int32_t* cu_seqlens, int32_t n_seqs,
+                     int32_t max_seq_len, const int32_t* rows, const int32_t* cu_rows,
+                     int32_t rows_per_layer, int32_t max_rows, const uint16_t* k_fresh,
+                     const uint16_t* v_fresh, uint16_t* k_cache, uint16_t* v_cache,
+                     uint16_t* v_cache_f16, void* plans, size_t plans_bytes, void* stream);
+
+/* Attention (Eq. 2) of layer `layer` of n_layers for the rows of S_layer, over
+ * the already patched cache: for every t in S_layer and query head h,
+ *   out[layer][t][h] = sum_{u = cu_seqlens[b]}^{t}
+ *                      softmax_u(scale * q[layer][t][h] . K[layer][g][u]) V[layer][g][u]
+ * with the arithmetic of kvb_sparse_attn.  Every pointer is the whole tensor
+ * as kvb_sparse_attn takes it (the call offsets to the layer).  v_cache_f16 is
+ * required (the fp16 shadow of V, current for every row, as kvb_stitch and
+ * kvb_patch keep it); plans as filled by kvb_patch with the same sizes on this
+ * device; workspace of at least kvb_sparse_attn_workspace_bytes(1, ...,
+ * v_f16_given = 1) bytes (partial records; calls that share it must be ordered
+ * on one stream).  Reads q, k_cache, v_cache_f16, rows, plans; writes out only.
+ * Errors: KVB_EINVAL (incl. layer outside [0, n_layers), plans or workspace
+ * too small, v_cache_f16 NULL), KVB_EUNSUPPORTED (as kvb_sparse_attn). */
+kvb_status kvb_sparse_attn_layer(int32_t layer, int32_t n_layers, int32_t n_q_heads,
+                                 int32_t n_kv_heads, int32_t head_dim, int64_t t_total,
+                                 const int32_t* cu_seqlens, int32_t n_seqs, int32_t max_seq_len,
+                                 const int32_t* rows, const int32_t* cu_rows,
+                                 int32_t rows_per_layer, int32_t max_rows, const uint16_t* q,
+                                 const uint16_t* k_cache, const uint16_t* v_cache_f16,
+                                 const void* plans, size_t plans_bytes, float softmax_scale,
+                                 kvb_dtype out_dtype, void* out, void* workspace,
+                                 size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

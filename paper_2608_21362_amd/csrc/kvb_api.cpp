@@ -72,7 +72,7 @@ kvb_status check_pool(const kvb_pool_layout* p) {
 
 extern "C" {
 
-int kvb_abi_version(void) { return 4; }
+int kvb_abi_version(void) { return 5; }
 
 const char* kvb_last_error(void) { return g_err.c_str(); }
 
@@ -383,14 +383,14 @@ size_t kvb_sparse_attn_workspace_bytes(int32_t n_layers, int32_t n_q_heads, int3
   return plan.workspace;
 }
 
-kvb_status kvb_sparse_attn(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads,
-                           int32_t head_dim, int64_t t_total, const int32_t* cu_seqlens,
-                           int32_t n_seqs, int32_t max_seq_len, const int32_t* rows,
-                           const int32_t* cu_rows, int32_t rows_per_layer, int32_t max_rows,
-                           const uint16_t* q, const uint16_t* k_fresh, const uint16_t* v_fresh,
-                           uint16_t* k_cache, uint16_t* v_cache, uint16_t* v_cache_f16,
-                           float softmax_scale, kvb_dtype out_dtype, void* out, void* workspace,
-                           size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Size checks shared by the attention entry points.
+kvb_status check_attn_sizes(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads,
+                            int32_t head_dim, int64_t t_total, int32_t n_seqs,
+                            int32_t max_seq_len, int32_t max_rows) {
   if (kvb_status s = check_head_dim(head_dim)) return s;
   REQUIRE(n_layers > 0 && n_q_heads > 0 && n_kv_heads > 0, "head counts and layers must be positive");
   REQUIRE(n_q_heads % n_kv_heads == 0, "n_q_heads %d not a multiple of n_kv_heads %d", n_q_heads,
@@ -403,6 +403,115 @@ kvb_status kvb_sparse_attn(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_hea
   REQUIRE(max_seq_len > 0 && max_seq_len <= t_total, "max_seq_len must be in (0, t_total]");
   REQUIRE(max_rows >= 0 && max_rows <= t_total, "max_rows must be in [0, t_total]");
   REQUIRE((int64_t)n_layers * n_kv_heads <= 65535, "n_layers * n_kv_heads > 65535");
+  return ok();
+}
+
+// Plan of one layer's attention launch (the fp16 shadow of V given).
+kvb_status layer_plan(int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int64_t t_total,
+                      int32_t n_seqs, int32_t max_seq_len, int32_t max_rows, kvb::AttnPlan* plan) {
+  if (!kvb::attn_plan(1, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs, max_seq_len, max_rows,
+                      true, plan))
+    return fail(KVB_EUNSUPPORTED, "too many attention work units (kv heads x row tiles x key blocks)");
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t kvb_attn_plans_bytes(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads,
+                            int32_t head_dim, int64_t t_total, int32_t n_seqs, int32_t max_seq_len,
+                            int32_t max_rows) {
+  if (n_layers <= 0 || n_q_heads <= 0 || n_kv_heads <= 0 || n_q_heads % n_kv_heads ||
+      head_dim <= 0 || t_total <= 0 || n_seqs <= 0 || max_seq_len <= 0 || max_rows < 0)
+    return 0;
+  kvb::AttnPlan plan;
+  if (!kvb::attn_plan(1, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs, max_seq_len, max_rows,
+                      true, &plan))
+    return 0;
+  return (size_t)n_layers * kvb::layer_plan_stride(plan);
+}
+
+kvb_status kvb_patch(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                     int64_t t_total, const int32_t* cu_seqlens, int32_t n_seqs,
+                     int32_t max_seq_len, const int32_t* rows, const int32_t* cu_rows,
+                     int32_t rows_per_layer, int32_t max_rows, const uint16_t* k_fresh,
+                     const uint16_t* v_fresh, uint16_t* k_cache, uint16_t* v_cache,
+                     uint16_t* v_cache_f16, void* plans, size_t plans_bytes, void* stream) {
+  if (kvb_status s = check_attn_sizes(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs,
+                                      max_seq_len, max_rows))
+    return s;
+  const void* ptrs[] = {cu_seqlens, rows, cu_rows};
+  for (const void* p : ptrs) REQUIRE(p != nullptr, "a required index pointer is NULL");
+  const void* tens[] = {k_fresh, v_fresh, k_cache, v_cache};
+  for (const void* p : tens) REQUIRE(p != nullptr && aligned16(p), "null or misaligned tensor");
+  if (v_cache_f16) REQUIRE(aligned16(v_cache_f16), "misaligned fp16 shadow of V");
+  kvb::AttnPlan plan;
+  if (kvb_status s = layer_plan(n_q_heads, n_kv_heads, head_dim, t_total, n_seqs, max_seq_len,
+                                max_rows, &plan))
+    return s;
+  if (plans) {
+    const size_t need = (size_t)n_layers * kvb::layer_plan_stride(plan);
+    REQUIRE(plans_bytes >= need, "plans %zu bytes, need %zu", plans_bytes, need);
+    REQUIRE(aligned16(plans), "misaligned plans");
+  }
+  if (max_rows == 0) return ok();
+  return hip_status(kvb::launch_patch_layers(plan, n_layers, n_kv_heads, head_dim, t_total,
+                                             cu_seqlens, n_seqs, rows, cu_rows, rows_per_layer,
+                                             max_rows, k_fresh, v_fresh, k_cache, v_cache,
+                                             v_cache_f16, plans, (hipStream_t)stream),
+                    "kvb_patch");
+}
+
+kvb_status kvb_sparse_attn_layer(int32_t layer, int32_t n_layers, int32_t n_q_heads,
+                                 int32_t n_kv_heads, int32_t head_dim, int64_t t_total,
+                                 const int32_t* cu_seqlens, int32_t n_seqs, int32_t max_seq_len,
+                                 const int32_t* rows, const int32_t* cu_rows,
+                                 int32_t rows_per_layer, int32_t max_rows, const uint16_t* q,
+                                 const uint16_t* k_cache, const uint16_t* v_cache_f16,
+                                 const void* plans, size_t plans_bytes, float softmax_scale,
+                                 kvb_dtype out_dtype, void* out, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  if (kvb_status s = check_attn_sizes(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs,
+                                      max_seq_len, max_rows))
+    return s;
+  REQUIRE(layer >= 0 && layer < n_layers, "layer %d outside [0, %d)", layer, n_layers);
+  REQUIRE(out_dtype == KVB_BF16 || out_dtype == KVB_F32, "out_dtype must be BF16 or F32");
+  REQUIRE(softmax_scale > 0.0f && isfinite(softmax_scale), "softmax_scale must be positive");
+  const void* ptrs[] = {cu_seqlens, rows, cu_rows};
+  for (const void* p : ptrs) REQUIRE(p != nullptr, "a required index pointer is NULL");
+  const void* tens[] = {q, k_cache, v_cache_f16, out, plans};
+  for (const void* p : tens)
+    REQUIRE(p != nullptr && aligned16(p), "null or misaligned tensor, shadow of V or plans");
+  kvb::AttnPlan plan;
+  if (kvb_status s = layer_plan(n_q_heads, n_kv_heads, head_dim, t_total, n_seqs, max_seq_len,
+                                max_rows, &plan))
+    return s;
+  const size_t need = (size_t)n_layers * kvb::layer_plan_stride(plan);
+  REQUIRE(plans_bytes >= need, "plans %zu bytes, need %zu", plans_bytes, need);
+  REQUIRE(workspace_bytes >= plan.workspace, "workspace %zu bytes, need %zu", workspace_bytes,
+          plan.workspace);
+  REQUIRE(workspace != nullptr && aligned16(workspace), "workspace NULL or misaligned");
+  if (max_rows == 0) return ok();
+  return hip_status(kvb::launch_sparse_attn_layer(plan, layer, n_q_heads, n_kv_heads, head_dim,
+                                                  t_total, cu_seqlens, n_seqs, rows, cu_rows,
+                                                  rows_per_layer, q, k_cache, v_cache_f16, plans,
+                                                  softmax_scale, out_dtype, out, workspace,
+                                                  (hipStream_t)stream),
+                    "kvb_sparse_attn_layer");
+}
+
+kvb_status kvb_sparse_attn(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads,
+                           int32_t head_dim, int64_t t_total, const int32_t* cu_seqlens,
+                           int32_t n_seqs, int32_t max_seq_len, const int32_t* rows,
+                           const int32_t* cu_rows, int32_t rows_per_layer, int32_t max_rows,
+                           const uint16_t* q, const uint16_t* k_fresh, const uint16_t* v_fresh,
+                           uint16_t* k_cache, uint16_t* v_cache, uint16_t* v_cache_f16,
+                           float softmax_scale, kvb_dtype out_dtype, void* out, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  if (kvb_status s = check_attn_sizes(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs,
+                                      max_seq_len, max_rows))
+    return s;
   REQUIRE(out_dtype == KVB_BF16 || out_dtype == KVB_F32, "out_dtype must be BF16 or F32");
   REQUIRE(softmax_scale > 0.0f && isfinite(softmax_scale), "softmax_scale must be positive");
   const void* ptrs[] = {cu_seqlens, rows, cu_rows};

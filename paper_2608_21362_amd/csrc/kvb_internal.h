@@ -75,4 +75,23 @@ hipError_t launch_sparse_attn(const AttnPlan& plan, int n_layers, int n_q_heads,
                               float softmax_scale, kvb_dtype out_dtype, void* out, void* workspace,
                               hipStream_t s);
 
+// Bytes of one layer's plan in a buffer of per-layer plans (a multiple of 256).
+size_t layer_plan_stride(const AttnPlan& layer_plan);
+// Patch of n_layers layers; with plans != NULL also the per-layer plans
+// (layer_plan is the one-layer plan, the fp16 shadow of V given).
+hipError_t launch_patch_layers(const AttnPlan& layer_plan, int n_layers, int n_kv_heads,
+                               int head_dim, int64_t t_total, const int32_t* cu_seqlens,
+                               int n_seqs, const int32_t* rows, const int32_t* cu_rows,
+                               int rows_per_layer, int max_rows, const uint16_t* k_fresh,
+                               const uint16_t* v_fresh, uint16_t* k_cache, uint16_t* v_cache,
+                               uint16_t* v_cache_f16, void* plans, hipStream_t s);
+// Attention of layer `layer` over the patched cache with its prebuilt plan.
+hipError_t launch_sparse_attn_layer(const AttnPlan& layer_plan, int layer, int n_q_heads,
+                                    int n_kv_heads, int head_dim, int64_t t_total,
+                                    const int32_t* cu_seqlens, int n_seqs, const int32_t* rows,
+                                    const int32_t* cu_rows, int rows_per_layer, const uint16_t* q,
+                                    const uint16_t* k_cache, const uint16_t* v_cache_f16,
+                                    const void* plans, float softmax_scale, kvb_dtype out_dtype,
+                                    void* out, void* workspace, hipStream_t s);
+
 }  // namespace kvb

@@ -701,7 +701,10 @@ __device__ __forceinline__ void build_plan(
 // Patch: cache[l][h][t] <- fresh[l][h][t] for every selected row t (both
 // tensors, every kv head; one wave per row), with the fp16 image of the new V
 // rows when the caller keeps an fp16 shadow of V.  With plan != NULL the first
-// workgroup builds the work decomposition instead.
+// n_plans workgroups build work decompositions instead: one plan over all L
+// layers (n_plans = 1), or one plan per layer (n_plans = L, plan p at
+// plan + p * plan_stride, over layer p's row set alone).  n_tiles counts the
+// tiles of one plan.
 __global__ void __launch_bounds__(256)
 patch_kernel(int32_t L, int32_t Hkv, int32_t D, int64_t t_total, int32_t n_seqs,
              const int32_t* __restrict__ rows, const int32_t* __restrict__ cu_rows,
@@ -710,15 +713,23 @@ patch_kernel(int32_t L, int32_t Hkv, int32_t D, int64_t t_total, int32_t n_seqs,
              uint16_t* __restrict__ vc, uint16_t* __restrict__ vh,
              const int32_t* __restrict__ cu_seqlens, int32_t n_tiles, int32_t tile_slots,
              int32_t rows_per_tile, int32_t n_wg, int32_t n_first, int32_t n_wg_max,
-             int32_t* __restrict__ plan) {
-  // the plan builder is workgroup 0: dispatched first, it starts its chain of
+             int32_t* __restrict__ plan, int32_t n_plans, int64_t plan_stride) {
+  // the plan builders come first: dispatched first, they start their chains of
   // dependent loads while the copying workgroups are still being dispatched
-  if (plan != nullptr && blockIdx.x == 0) {
-    build_plan(n_tiles, tile_slots, Hkv, t_total, cu_seqlens, n_seqs, rows, cu_rows,
-               rows_per_layer, rows_per_tile, n_wg, n_first, n_wg_max, plan);
+  if (plan != nullptr && (int)blockIdx.x < n_plans) {
+    const int p = blockIdx.x;
+    if (n_plans == 1) {
+      build_plan(n_tiles, tile_slots, Hkv, t_total, cu_seqlens, n_seqs, rows, cu_rows,
+                 rows_per_layer, rows_per_tile, n_wg, n_first, n_wg_max, plan);
+    } else {
+      const int64_t set = rows_per_layer ? p : 0;
+      build_plan(n_tiles, tile_slots, Hkv, t_total, cu_seqlens, n_seqs, rows + set * t_total,
+                 cu_rows + set * (n_seqs + 1), 0, rows_per_tile, n_wg, n_first, n_wg_max,
+                 plan + p * plan_stride);
+    }
     return;
   }
-  const int64_t copy_block = (int64_t)blockIdx.x - (plan != nullptr ? 1 : 0);
+  const int64_t copy_block = (int64_t)blockIdx.x - (plan != nullptr ? n_plans : 0);
   const int64_t wave = (copy_block * blockDim.x + threadIdx.x) >> 6;
   const int lane = threadIdx.x & 63;
   const int64_t l = wave / max_rows;
@@ -962,49 +973,54 @@ bool attn_plan(int n_layers, int n_q_heads, int n_kv_heads, int head_dim, int64_
   return true;
 }
 
-hipError_t launch_sparse_attn(const AttnPlan& plan, int n_layers, int n_q_heads, int n_kv_heads,
-                              int head_dim, int64_t t_total, const int32_t* cu_seqlens,
-                              int n_seqs, const int32_t* rows, const int32_t* cu_rows,
-                              int rows_per_layer, int max_rows, const uint16_t* q,
-                              const uint16_t* k_fresh, const uint16_t* v_fresh,
-                              uint16_t* k_cache, uint16_t* v_cache, uint16_t* v_cache_f16,
-                              float softmax_scale, kvb_dtype out_dtype, void* out, void* workspace,
-                              hipStream_t s) {
-  char* wsb = reinterpret_cast<char*>(workspace);
-  uint16_t* v16 = plan.v16_in_ws ? reinterpret_cast<uint16_t*>(wsb + plan.v16_offset) : v_cache_f16;
-  int32_t* wplan = reinterpret_cast<int32_t*>(wsb + plan.plan_offset);
-  float* parts = reinterpret_cast<float*>(wsb + plan.parts_offset);
-  int n_wg = resident_workgroups();
-  if (n_wg > plan.n_wg_max) n_wg = plan.n_wg_max;
+namespace {
+
+// Attention workgroups and first-slot workgroups of a launch on this device.
+void launch_shape(const AttnPlan& plan, int* n_wg, int* n_first) {
+  int w = resident_workgroups();
+  if (w > plan.n_wg_max) w = plan.n_wg_max;
   // first-slot workgroups (see kFirstShareNum) exist only with two per CU
-  const int n_first = (KVB_ATTN_WG_PER_CU == 2 && n_wg == resident_workgroups()) ? n_wg / 2 : 0;
-  // enough tiles to keep every resident workgroup busy twice over: one tile per
-  // workgroup, no partials; otherwise balanced ranges
-  const int balanced = plan.n_tiles < 2 * n_wg;
-  {
-    const int64_t waves = (int64_t)n_layers * max_rows;
-    const int64_t blocks = (waves * 64 + 255) / 256 + (balanced ? 1 : 0);
-    if (blocks > 0)
-      hipLaunchKernelGGL(patch_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n_layers,
-                         n_kv_heads, head_dim, t_total, n_seqs, rows, cu_rows, rows_per_layer,
-                         max_rows, k_fresh, v_fresh, k_cache, v_cache,
-                         plan.v16_in_ws ? nullptr : v_cache_f16, cu_seqlens, plan.n_tiles,
-                         plan.tile_slots, plan.rows_per_tile, n_wg, n_first, plan.n_wg_max,
-                         balanced ? wplan : nullptr);
-  }
-  if (plan.v16_in_ws) {
-    const int64_t n8 = (int64_t)n_layers * n_kv_heads * t_total * head_dim / 8;
-    int64_t blocks = (n8 + 255) / 256;
-    if (blocks > 8192) blocks = 8192;
-    hipLaunchKernelGGL(v16_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n8, v_cache, v16);
-  }
+  *n_first = (KVB_ATTN_WG_PER_CU == 2 && w == resident_workgroups()) ? w / 2 : 0;
+  *n_wg = w;
+}
+
+// Enough tiles to keep every resident workgroup busy twice over: one tile per
+// workgroup, no partial records; otherwise balanced ranges.
+bool is_balanced(const AttnPlan& plan, int n_wg) { return plan.n_tiles < 2 * n_wg; }
+
+// Patch launch: copies the selected rows of n_layers layers; with plans != NULL
+// its first n_plans workgroups build the plans (see patch_kernel).
+void launch_patch(int n_layers, int n_kv_heads, int head_dim, int64_t t_total,
+                  const int32_t* cu_seqlens, int n_seqs, const int32_t* rows,
+                  const int32_t* cu_rows, int rows_per_layer, int max_rows,
+                  const uint16_t* k_fresh, const uint16_t* v_fresh, uint16_t* k_cache,
+                  uint16_t* v_cache, uint16_t* v_f16, const AttnPlan& plan, int n_wg, int n_first,
+                  int32_t* plans, int n_plans, int64_t plan_stride, hipStream_t s) {
+  const int64_t waves = (int64_t)n_layers * max_rows;
+  const int64_t blocks = (waves * 64 + 255) / 256 + (plans ? n_plans : 0);
+  if (blocks > 0)
+    hipLaunchKernelGGL(patch_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n_layers, n_kv_heads,
+                       head_dim, t_total, n_seqs, rows, cu_rows, rows_per_layer, max_rows, k_fresh,
+                       v_fresh, k_cache, v_cache, v_f16, cu_seqlens, plan.n_tiles, plan.tile_slots,
+                       plan.rows_per_tile, n_wg, n_first, plan.n_wg_max, plans, n_plans,
+                       plan_stride);
+}
+
+// Attention (and, for balanced ranges, the merge of cut tiles) over an already
+// patched cache; wplan is the plan of exactly these layers.
+void launch_attend(const AttnPlan& plan, int n_wg, bool balanced, int n_q_heads, int n_kv_heads,
+                   int head_dim, int64_t t_total, const int32_t* cu_seqlens, int n_seqs,
+                   const int32_t* rows, const int32_t* cu_rows, int rows_per_layer,
+                   const uint16_t* q, const uint16_t* k_cache, const uint16_t* v16,
+                   float softmax_scale, kvb_dtype out_dtype, void* out, const int32_t* wplan,
+                   float* parts, hipStream_t s) {
   const int log2g = ilog2(n_q_heads / n_kv_heads);
   const float c_log2 = softmax_scale * 1.4426950408889634f;
   const int out_f32 = out_dtype == KVB_F32;
   const dim3 grid(balanced ? n_wg : plan.n_tiles);
 #define KVB_ATTN(D)                                                                              \
-  hipLaunchKernelGGL(attn_kernel<D>, grid, dim3(kThreads), 0, s, balanced, plan.n_tiles, n_q_heads,\
-                     n_kv_heads, log2g, t_total, cu_seqlens, n_seqs, rows, cu_rows,              \
+  hipLaunchKernelGGL(attn_kernel<D>, grid, dim3(kThreads), 0, s, (int)balanced, plan.n_tiles,     \
+                     n_q_heads, n_kv_heads, log2g, t_total, cu_seqlens, n_seqs, rows, cu_rows,    \
                      rows_per_layer, plan.rows_per_tile, plan.tile_slots, wplan, plan.n_wg_max,   \
                      plan.n_rec, q, k_cache, v16, c_log2, out_f32, out, parts)
 #define KVB_COMBINE(D)                                                                           \
@@ -1020,6 +1036,86 @@ hipError_t launch_sparse_attn(const AttnPlan& plan, int n_layers, int n_q_heads,
   }
 #undef KVB_ATTN
 #undef KVB_COMBINE
+}
+
+}  // namespace
+
+hipError_t launch_sparse_attn(const AttnPlan& plan, int n_layers, int n_q_heads, int n_kv_heads,
+                              int head_dim, int64_t t_total, const int32_t* cu_seqlens,
+                              int n_seqs, const int32_t* rows, const int32_t* cu_rows,
+                              int rows_per_layer, int max_rows, const uint16_t* q,
+                              const uint16_t* k_fresh, const uint16_t* v_fresh,
+                              uint16_t* k_cache, uint16_t* v_cache, uint16_t* v_cache_f16,
+                              float softmax_scale, kvb_dtype out_dtype, void* out, void* workspace,
+                              hipStream_t s) {
+  char* wsb = reinterpret_cast<char*>(workspace);
+  uint16_t* v16 = plan.v16_in_ws ? reinterpret_cast<uint16_t*>(wsb + plan.v16_offset) : v_cache_f16;
+  int32_t* wplan = reinterpret_cast<int32_t*>(wsb + plan.plan_offset);
+  float* parts = reinterpret_cast<float*>(wsb + plan.parts_offset);
+  int n_wg = 0, n_first = 0;
+  launch_shape(plan, &n_wg, &n_first);
+  const bool balanced = is_balanced(plan, n_wg);
+  launch_patch(n_layers, n_kv_heads, head_dim, t_total, cu_seqlens, n_seqs, rows, cu_rows,
+               rows_per_layer, max_rows, k_fresh, v_fresh, k_cache, v_cache,
+               plan.v16_in_ws ? nullptr : v_cache_f16, plan, n_wg, n_first,
+               balanced ? wplan : nullptr, 1, 0, s);
+  if (plan.v16_in_ws) {
+    const int64_t n8 = (int64_t)n_layers * n_kv_heads * t_total * head_dim / 8;
+    int64_t blocks = (n8 + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    hipLaunchKernelGGL(v16_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n8, v_cache, v16);
+  }
+  launch_attend(plan, n_wg, balanced, n_q_heads, n_kv_heads, head_dim, t_total, cu_seqlens, n_seqs,
+                rows, cu_rows, rows_per_layer, q, k_cache, v16, softmax_scale, out_dtype, out,
+                wplan, parts, s);
+  return hipGetLastError();
+}
+
+size_t layer_plan_stride(const AttnPlan& layer_plan) {
+  const size_t ints = (size_t)tile_meta_offset(layer_plan.n_tiles, layer_plan.n_wg_max) +
+                      4 * (size_t)layer_plan.n_tiles;
+  return ((ints * sizeof(int32_t) + 255) / 256) * 256;
+}
+
+hipError_t launch_patch_layers(const AttnPlan& layer_plan, int n_layers, int n_kv_heads,
+                               int head_dim, int64_t t_total, const int32_t* cu_seqlens,
+                               int n_seqs, const int32_t* rows, const int32_t* cu_rows,
+                               int rows_per_layer, int max_rows, const uint16_t* k_fresh,
+                               const uint16_t* v_fresh, uint16_t* k_cache, uint16_t* v_cache,
+                               uint16_t* v_cache_f16, void* plans, hipStream_t s) {
+  int n_wg = 0, n_first = 0;
+  launch_shape(layer_plan, &n_wg, &n_first);
+  // plans are needed (and built) only for balanced ranges
+  int32_t* p = (plans && is_balanced(layer_plan, n_wg)) ? reinterpret_cast<int32_t*>(plans) : nullptr;
+  launch_patch(n_layers, n_kv_heads, head_dim, t_total, cu_seqlens, n_seqs, rows, cu_rows,
+               rows_per_layer, max_rows, k_fresh, v_fresh, k_cache, v_cache, v_cache_f16,
+               layer_plan, n_wg, n_first, p, n_layers,
+               (int64_t)(layer_plan_stride(layer_plan) / sizeof(int32_t)), s);
+  return hipGetLastError();
+}
+
+hipError_t launch_sparse_attn_layer(const AttnPlan& layer_plan, int layer, int n_q_heads,
+                                    int n_kv_heads, int head_dim, int64_t t_total,
+                                    const int32_t* cu_seqlens, int n_seqs, const int32_t* rows,
+                                    const int32_t* cu_rows, int rows_per_layer, const uint16_t* q,
+                                    const uint16_t* k_cache, const uint16_t* v_cache_f16,
+                                    const void* plans, float softmax_scale, kvb_dtype out_dtype,
+                                    void* out, void* workspace, hipStream_t s) {
+  int n_wg = 0, n_first = 0;
+  launch_shape(layer_plan, &n_wg, &n_first);
+  const bool balanced = is_balanced(layer_plan, n_wg);
+  const int64_t set = rows_per_layer ? layer : 0;
+  const int64_t kv = (int64_t)layer * n_kv_heads * t_total * head_dim;
+  const int64_t qo = (int64_t)layer * t_total * n_q_heads * head_dim;
+  const int32_t* wplan = reinterpret_cast<const int32_t*>(
+      reinterpret_cast<const char*>(plans) + (size_t)layer * layer_plan_stride(layer_plan));
+  float* parts = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + layer_plan.parts_offset);
+  void* out_l = out_dtype == KVB_F32 ? (void*)(reinterpret_cast<float*>(out) + qo)
+                                     : (void*)(reinterpret_cast<uint16_t*>(out) + qo);
+  launch_attend(layer_plan, n_wg, balanced, n_q_heads, n_kv_heads, head_dim, t_total, cu_seqlens,
+                n_seqs, rows + set * t_total, cu_rows + set * (n_seqs + 1), 0, q + qo,
+                k_cache + kv, v_cache_f16 + kv, softmax_scale, out_dtype, out_l,
+                balanced ? wplan : nullptr, parts, s);
   return hipGetLastError();
 }
 

@@ -65,6 +65,12 @@ _SIGS = {
     "kvb_sparse_attn": (_i32, [_i32, _i32, _i32, _i32, _i64, _vp, _i32, _i32, _vp, _vp, _i32,
                                _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _i32, _vp, _vp, _sz,
                                _vp]),
+    "kvb_attn_plans_bytes": (_sz, [_i32, _i32, _i32, _i32, _i64, _i32, _i32, _i32]),
+    "kvb_patch": (_i32, [_i32, _i32, _i32, _i32, _i64, _vp, _i32, _i32, _vp, _vp, _i32, _i32,
+                         _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "kvb_sparse_attn_layer": (_i32, [_i32, _i32, _i32, _i32, _i32, _i64, _vp, _i32, _i32, _vp,
+                                     _vp, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _f32, _i32, _vp,
+                                     _vp, _sz, _vp]),
 }
 
 
@@ -239,3 +245,30 @@ def kvb_sparse_attn(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, cu_seqle
                                 _p(k_cache), _p(v_cache), _p(v_cache_f16), float(softmax_scale),
                                 out_dtype, _p(out), _p(workspace), workspace_bytes,
                                 _stream(stream)))
+
+
+def kvb_attn_plans_bytes(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs, max_seq_len,
+                         max_rows) -> int:
+    return _lib.kvb_attn_plans_bytes(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs,
+                                     max_seq_len, max_rows)
+
+
+def kvb_patch(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, cu_seqlens, n_seqs,
+              max_seq_len, rows, cu_rows, rows_per_layer, max_rows, k_fresh, v_fresh, k_cache,
+              v_cache, v_cache_f16, plans, plans_bytes, stream=None):
+    _check(_lib.kvb_patch(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, _p(cu_seqlens),
+                          n_seqs, max_seq_len, _p(rows), _p(cu_rows), int(rows_per_layer),
+                          max_rows, _p(k_fresh), _p(v_fresh), _p(k_cache), _p(v_cache),
+                          _p(v_cache_f16), _p(plans), plans_bytes, _stream(stream)))
+
+
+def kvb_sparse_attn_layer(layer, n_layers, n_q_heads, n_kv_heads, head_dim, t_total, cu_seqlens,
+                          n_seqs, max_seq_len, rows, cu_rows, rows_per_layer, max_rows, q,
+                          k_cache, v_cache_f16, plans, plans_bytes, softmax_scale, out_dtype,
+                          out, workspace, workspace_bytes, stream=None):
+    _check(_lib.kvb_sparse_attn_layer(layer, n_layers, n_q_heads, n_kv_heads, head_dim, t_total,
+                                      _p(cu_seqlens), n_seqs, max_seq_len, _p(rows), _p(cu_rows),
+                                      int(rows_per_layer), max_rows, _p(q), _p(k_cache),
+                                      _p(v_cache_f16), _p(plans), plans_bytes,
+                                      float(softmax_scale), out_dtype, _p(out), _p(workspace),
+                                      workspace_bytes, _stream(stream)))

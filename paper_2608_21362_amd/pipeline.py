@@ -156,7 +156,7 @@ def populate(w: kw.Workload, s: kw.Structure, layers=None, with_q=True, draws_fn
 class PathBuffers:
     k_cache: torch.Tensor
     v_cache: torch.Tensor
-    v_cache_f16: torch.Tensor  # fp16 shadow of v_cache, kept by kvb_stitch and kvb_sparse_attn
+    v_cache_f16: torch.Tensor  # fp16 shadow of v_cache, kept by kvb_stitch and the patch
     delta: torch.Tensor
     rows: torch.Tensor
     cu_rows: torch.Tensor
@@ -166,6 +166,8 @@ class PathBuffers:
     sel_ws_bytes: int
     attn_ws_bytes: int
     attn_ws_bytes_all: int = 0
+    plans: torch.Tensor = None  # per-layer attention plans written by kvb_patch
+    plans_bytes: int = 0
 
 
 def buffers(di: DeviceInputs, out_dtype=kvb.KVB_BF16, attn_all_layers=False) -> PathBuffers:
@@ -177,6 +179,8 @@ def buffers(di: DeviceInputs, out_dtype=kvb.KVB_BF16, attn_all_layers=False) -> 
     all_ws = kvb.kvb_sparse_attn_workspace_bytes(L, w.n_q_heads, w.n_kv_heads, w.head_dim, T, B,
                                                  di.max_seq_len, di.max_rows, 1)
     attn_bytes = max(per_layer_ws, all_ws if attn_all_layers else 0)
+    plans_bytes = kvb.kvb_attn_plans_bytes(L, w.n_q_heads, w.n_kv_heads, w.head_dim, T, B,
+                                           di.max_seq_len, di.max_rows)
     odt = torch.int16 if out_dtype == kvb.KVB_BF16 else torch.float32
     out = torch.full((L, T, w.n_q_heads, w.head_dim), -1, dtype=odt, device="cuda")
     if out_dtype == kvb.KVB_BF16:
@@ -194,7 +198,9 @@ def buffers(di: DeviceInputs, out_dtype=kvb.KVB_BF16, attn_all_layers=False) -> 
         out=out,
         sel_ws=torch.empty(max(sel_bytes, 16), dtype=torch.uint8, device="cuda"),
         attn_ws=torch.empty(max(attn_bytes, 16), dtype=torch.uint8, device="cuda"),
-        sel_ws_bytes=sel_bytes, attn_ws_bytes=per_layer_ws, attn_ws_bytes_all=all_ws)
+        sel_ws_bytes=sel_bytes, attn_ws_bytes=per_layer_ws, attn_ws_bytes_all=all_ws,
+        plans=torch.empty(max(plans_bytes, 16), dtype=torch.uint8, device="cuda"),
+        plans_bytes=plans_bytes)
 
 
 def stitch(di: DeviceInputs, pb: PathBuffers, out_dtype=kvb.KVB_BF16, k_out=None, v_out=None,
@@ -252,6 +258,29 @@ def sparse_attn_layer(di: DeviceInputs, pb: PathBuffers, i: int, out_dtype=kvb.K
                         pb.attn_ws_bytes, stream)
 
 
+def patch(di: DeviceInputs, pb: PathBuffers, stream=None):
+    """Alg. 2 step 4 for every populated layer in one launch, which also builds
+    the per-layer attention plans that ``attn_layer`` reads."""
+    w, T = di.w, di.w.t_total
+    B = len(di.s.cu_seqlens) - 1
+    kvb.kvb_patch(di.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, T, di.cu_seqlens, B,
+                  di.max_seq_len, pb.rows, pb.cu_rows, int(w.per_layer), di.max_rows,
+                  di.k_fresh, di.v_fresh, pb.k_cache, pb.v_cache, pb.v_cache_f16, pb.plans,
+                  pb.plans_bytes, stream)
+
+
+def attn_layer(di: DeviceInputs, pb: PathBuffers, i: int, out_dtype=kvb.KVB_BF16, stream=None):
+    """Attention of populated layer ``i`` over the cache ``patch`` left (the
+    repair forward's per-layer launch: attention and the merge of cut tiles)."""
+    w, T = di.w, di.w.t_total
+    B = len(di.s.cu_seqlens) - 1
+    kvb.kvb_sparse_attn_layer(i, di.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, T,
+                              di.cu_seqlens, B, di.max_seq_len, pb.rows, pb.cu_rows,
+                              int(w.per_layer), di.max_rows, di.q, pb.k_cache, pb.v_cache_f16,
+                              pb.plans, pb.plans_bytes, 1.0 / float(np.sqrt(w.head_dim)),
+                              out_dtype, pb.out, pb.attn_ws, pb.attn_ws_bytes, stream)
+
+
 def sparse_attn_all(di: DeviceInputs, pb: PathBuffers, out_dtype=kvb.KVB_BF16, stream=None):
     """Attention of every populated layer in one launch."""
     w, T = di.w, di.w.t_total
@@ -264,9 +293,11 @@ def sparse_attn_all(di: DeviceInputs, pb: PathBuffers, out_dtype=kvb.KVB_BF16, s
 
 
 def run_path(di: DeviceInputs, pb: PathBuffers, attn_all_layers=False, out_dtype=kvb.KVB_BF16,
-             stream=None):
+             stream=None, patch_once=True):
     """One pass of the whole path over the batch.  With no prompt above the
-    probe threshold the deviation pass is skipped (every top-k is empty)."""
+    probe threshold the deviation pass is skipped (every top-k is empty).
+    Attention: one launch for every layer (attn_all_layers), or layer by layer,
+    after one patch of every layer (patch_once) or with a patch per layer."""
     stitch(di, pb, stream=stream)
     if di.n_probed:
         deviation_topk(di, pb, stream=stream)
@@ -274,6 +305,10 @@ def run_path(di: DeviceInputs, pb: PathBuffers, attn_all_layers=False, out_dtype
         select(di, pb, stream=stream)
     if attn_all_layers:
         sparse_attn_all(di, pb, out_dtype, stream)
+    elif patch_once:
+        patch(di, pb, stream=stream)
+        for i in range(di.n_layers):
+            attn_layer(di, pb, i, out_dtype, stream)
     else:
         for i in range(di.n_layers):
             sparse_attn_layer(di, pb, i, out_dtype, stream)

@@ -104,8 +104,9 @@ def run(n_requests=40, seed=0, n_layers=36, probe_min_pct=0, log=print):
             elif di.n_pool:
                 pipeline.stitch(di, pb)
             pipeline.select(di, pb)
+            pipeline.patch(di, pb)
             for li in range(di.n_layers):
-                pipeline.sparse_attn_layer(di, pb, li)
+                pipeline.attn_layer(di, pb, li)
 
         def timed(fn):
             a = torch.cuda.Event(enable_timing=True)

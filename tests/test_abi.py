@@ -33,7 +33,7 @@ def test_every_declared_symbol_is_exported():
     for n in names:
         assert hasattr(lib, n), n
     assert sorted(names) == sorted(kvb.EXPORTED)
-    assert kvb.kvb_abi_version() == 4
+    assert kvb.kvb_abi_version() == 5
 
 
 def test_ceiling_library_loads():
@@ -241,6 +241,92 @@ def test_sparse_attn_rejects(over, status):
     with pytest.raises(kvb.KvbError) as e:
         _attn(**over)
     assert e.value.status == status
+
+
+def _plans_bytes(a):
+    return kvb.kvb_attn_plans_bytes(a["n_layers"], a["n_q_heads"], a["n_kv_heads"],
+                                    max(a["head_dim"], 1), a["t_total"], max(a["n_seqs"], 1),
+                                    max(a["max_seq_len"], 1), a["max_rows"])
+
+
+def _patch(**over):
+    args = dict(n_layers=4, n_q_heads=16, n_kv_heads=2, head_dim=128, t_total=4096,
+                cu_seqlens=FAKE, n_seqs=1, max_seq_len=4096, rows=FAKE, cu_rows=FAKE,
+                rows_per_layer=1, max_rows=600, k_fresh=FAKE, v_fresh=FAKE, k_cache=FAKE,
+                v_cache=FAKE, v_cache_f16=FAKE, plans=FAKE, plans_bytes=None, stream=0)
+    args.update(over)
+    if args["plans_bytes"] is None:
+        args["plans_bytes"] = _plans_bytes(args)
+    kvb.kvb_patch(**args)
+
+
+def _attn_layer(**over):
+    args = dict(layer=2, n_layers=4, n_q_heads=16, n_kv_heads=2, head_dim=128, t_total=4096,
+                cu_seqlens=FAKE, n_seqs=1, max_seq_len=4096, rows=FAKE, cu_rows=FAKE,
+                rows_per_layer=1, max_rows=600, q=FAKE, k_cache=FAKE, v_cache_f16=FAKE,
+                plans=FAKE, plans_bytes=None, softmax_scale=0.088, out_dtype=kvb.KVB_BF16,
+                out=FAKE, workspace=FAKE, workspace_bytes=None, stream=0)
+    args.update(over)
+    if args["plans_bytes"] is None:
+        args["plans_bytes"] = _plans_bytes(args)
+    if args["workspace_bytes"] is None:
+        args["workspace_bytes"] = kvb.kvb_sparse_attn_workspace_bytes(
+            1, args["n_q_heads"], args["n_kv_heads"], max(args["head_dim"], 1), args["t_total"],
+            max(args["n_seqs"], 1), max(args["max_seq_len"], 1), args["max_rows"], 1)
+    kvb.kvb_sparse_attn_layer(**args)
+
+
+def test_plans_bytes_is_pure_and_per_layer():
+    one = kvb.kvb_attn_plans_bytes(1, 16, 2, 128, 8192, 1, 8192, 1228)
+    assert one > 0 and one % 256 == 0
+    assert kvb.kvb_attn_plans_bytes(36, 16, 2, 128, 8192, 1, 8192, 1228) == 36 * one
+    assert kvb.kvb_attn_plans_bytes(1, 16, 3, 128, 8192, 1, 8192, 1228) == 0
+    assert kvb.kvb_attn_plans_bytes(0, 16, 2, 128, 8192, 1, 8192, 1228) == 0
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(n_kv_heads=3), kvb.KVB_EINVAL),
+    (dict(n_q_heads=24, n_kv_heads=4), kvb.KVB_EUNSUPPORTED),
+    (dict(head_dim=256), kvb.KVB_EUNSUPPORTED),
+    (dict(plans_bytes=16), kvb.KVB_EINVAL),
+    (dict(plans=FAKE + 2), kvb.KVB_EINVAL),
+    (dict(k_fresh=None), kvb.KVB_EINVAL),
+    (dict(v_cache=FAKE + 2), kvb.KVB_EINVAL),
+    (dict(rows=None), kvb.KVB_EINVAL),
+    (dict(max_rows=5000), kvb.KVB_EINVAL),
+    (dict(v_cache_f16=FAKE + 2), kvb.KVB_EINVAL),
+])
+def test_patch_rejects(over, status):
+    with pytest.raises(kvb.KvbError) as e:
+        _patch(**over)
+    assert e.value.status == status
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(layer=4), kvb.KVB_EINVAL),
+    (dict(layer=-1), kvb.KVB_EINVAL),
+    (dict(n_kv_heads=3), kvb.KVB_EINVAL),
+    (dict(n_q_heads=128, n_kv_heads=2), kvb.KVB_EUNSUPPORTED),
+    (dict(v_cache_f16=None), kvb.KVB_EINVAL),
+    (dict(plans=None), kvb.KVB_EINVAL),
+    (dict(plans_bytes=16), kvb.KVB_EINVAL),
+    (dict(workspace_bytes=1), kvb.KVB_EINVAL),
+    (dict(workspace=None), kvb.KVB_EINVAL),
+    (dict(q=FAKE + 2), kvb.KVB_EINVAL),
+    (dict(softmax_scale=float("nan")), kvb.KVB_EINVAL),
+    (dict(out_dtype=7), kvb.KVB_EINVAL),
+])
+def test_sparse_attn_layer_rejects(over, status):
+    with pytest.raises(kvb.KvbError) as e:
+        _attn_layer(**over)
+    assert e.value.status == status
+
+
+def test_patch_and_layer_without_rows_are_no_ops():
+    """max_rows = 0: nothing to patch or attend; both calls return before any
+    device work (so they succeed here, with no GPU)."""
+    _patch(max_rows=0)
+    _attn_layer(max_rows=0)
 
 
 def test_chunk_importance_rejects():

@@ -65,13 +65,18 @@ def test_select_empty_and_tiny_prompts():
             assert g_cu[si, b] == g_cu[si, b + 1]
 
 
-@pytest.mark.parametrize("hq,hkv,d,shadow", [(16, 2, 128, True), (16, 2, 128, False),
-                                            (4, 2, 64, True), (8, 8, 64, False)])
-def test_attention_ragged_with_empty_prompts(hq, hkv, d, shadow):
+@pytest.mark.parametrize("hq,hkv,d,shadow,split", [(16, 2, 128, True, False),
+                                                  (16, 2, 128, False, False),
+                                                  (4, 2, 64, True, False),
+                                                  (8, 8, 64, False, False),
+                                                  (16, 2, 128, True, True),
+                                                  (4, 2, 64, True, True)])
+def test_attention_ragged_with_empty_prompts(hq, hkv, d, shadow, split):
+    """split: kvb_patch, then kvb_sparse_attn_layer (instead of one kvb_sparse_attn)."""
     _need_gpu()
     from paper_2608_21362_amd import kvb
 
-    _say(f"[edges] attention Hq={hq} Hkv={hkv} d={d} shadow={shadow}")
+    _say(f"[edges] attention Hq={hq} Hkv={hkv} d={d} shadow={shadow} split={split}")
     rng = np.random.default_rng(hq * 100 + d + shadow)
     cu = np.concatenate([[0], np.cumsum(LENS)]).astype(np.int32)
     T, B = int(cu[-1]), len(LENS)
@@ -99,12 +104,20 @@ def test_attention_ragged_with_empty_prompts(hq, hkv, d, shadow):
     out = torch.full((T, hq, d), -1, dtype=torch.int16, device="cuda")
     wsb = kvb.kvb_sparse_attn_workspace_bytes(1, hq, hkv, d, T, B, max_seq, len(rows), int(shadow))
     ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
-    kvb.kvb_sparse_attn(1, hq, hkv, d, T, torch.from_numpy(cu).cuda(), B, max_seq,
-                        torch.from_numpy(rows).cuda(), torch.from_numpy(cu_rows).cuda(), 0,
-                        len(rows), torch.from_numpy(q.view(np.int16)).cuda(),
-                        torch.from_numpy(kf.view(np.int16)).cuda(),
-                        torch.from_numpy(vf.view(np.int16)).cuda(), dk, dv, v16,
-                        1.0 / np.sqrt(d), kvb.KVB_BF16, out, ws, wsb)
+    dcu, drows, dcur = (torch.from_numpy(x).cuda() for x in (cu, rows, cu_rows))
+    dq = torch.from_numpy(q.view(np.int16)).cuda()
+    dkf, dvf = torch.from_numpy(kf.view(np.int16)).cuda(), torch.from_numpy(vf.view(np.int16)).cuda()
+    if split:
+        pbytes = kvb.kvb_attn_plans_bytes(1, hq, hkv, d, T, B, max_seq, len(rows))
+        plans = torch.empty(max(pbytes, 16), dtype=torch.uint8, device="cuda")
+        kvb.kvb_patch(1, hq, hkv, d, T, dcu, B, max_seq, drows, dcur, 0, len(rows), dkf, dvf, dk,
+                      dv, v16, plans, pbytes)
+        kvb.kvb_sparse_attn_layer(0, 1, hq, hkv, d, T, dcu, B, max_seq, drows, dcur, 0, len(rows),
+                                  dq, dk, v16, plans, pbytes, 1.0 / np.sqrt(d), kvb.KVB_BF16, out,
+                                  ws, wsb)
+    else:
+        kvb.kvb_sparse_attn(1, hq, hkv, d, T, dcu, B, max_seq, drows, dcur, 0, len(rows), dq, dkf,
+                            dvf, dk, dv, v16, 1.0 / np.sqrt(d), kvb.KVB_BF16, out, ws, wsb)
     torch.cuda.synchronize()
     pk, pv = oatt.patch(kc, kf, rows), oatt.patch(vc, vf, rows)
     assert np.array_equal(dk.cpu().numpy().view(np.uint16), pk)
