@@ -359,7 +359,8 @@ size_t kvb_attn_plans_bytes(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_he
  * Layouts and sizes as kvb_sparse_attn.  When plans is not NULL the same launch
  * also writes the attention work plan of every layer into it (at least
  * kvb_attn_plans_bytes bytes, 16-byte aligned; the contents are opaque), for
- * the kvb_sparse_attn_layer calls that follow on the same rows.
+ * the kvb_sparse_attn_layer calls that follow on the same rows.  Rows of S_l
+ * must be ascending within each prompt and belong to it (as kvb_sparse_attn).
  * Errors: KVB_EINVAL (incl. plans smaller than kvb_attn_plans_bytes),
  * KVB_EUNSUPPORTED (as kvb_sparse_attn). */
 kvb_status kvb_patch(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
@@ -379,7 +380,8 @@ kvb_status kvb_patch(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, in
  * kvb_patch keep it); plans as filled by kvb_patch with the same sizes on this
  * device; workspace of at least kvb_sparse_attn_workspace_bytes(1, ...,
  * v_f16_given = 1) bytes (partial records; calls that share it must be ordered
- * on one stream).  Reads q, k_cache, v_cache_f16, rows, plans; writes out only.
+ * on one stream).  Reads q, k_cache, v_cache_f16, rows, plans; writes out (rows
+ * of S_layer only) and the workspace.
  * Errors: KVB_EINVAL (incl. layer outside [0, n_layers), plans or workspace
  * too small, v_cache_f16 NULL), KVB_EUNSUPPORTED (as kvb_sparse_attn). */
 kvb_status kvb_sparse_attn_layer(int32_t layer, int32_t n_layers, int32_t n_q_heads,

@@ -1,8 +1,9 @@
 """Full-size GPU parity: the 36-layer 8K workload on every layer, the batched
 16 x 2048 workload, and three layers of the 36-layer 32K workload at their
 full per-layer size, in the launch configuration bench.py times (one fused
-stitch + deviation and one selection for all populated layers, then one
-attention call per layer with the fp16 shadow of V); the 8K workload also in
+stitch + deviation and one selection for all populated layers, one patch of
+every layer, then one attention call per layer with the fp16 shadow of V); the
+8K workload also in
 bench.py's --unfused configuration (one stitch, then one deviation +
 selection).
 
@@ -80,8 +81,11 @@ def test_fullsize(name, layers, n_sample, full, fused):
         pipeline.stitch(dev, pb)
         st_k, st_v, st_v16 = pb.k_cache.clone(), pb.v_cache.clone(), pb.v_cache_f16.clone()
         pipeline.deviation_topk(dev, pb)
+    # the launch configuration bench.py times: one patch of every layer, then
+    # one attention call per layer
+    pipeline.patch(dev, pb)
     for i in range(L):
-        pipeline.sparse_attn_layer(dev, pb, i)
+        pipeline.attn_layer(dev, pb, i)
     torch.cuda.synchronize()
     _say(f"[fullsize] {name}: GPU path done")
     rows_all = pb.rows.cpu().numpy()

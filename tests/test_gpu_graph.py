@@ -17,10 +17,12 @@ import kvb_workload as kw
 pytestmark = pytest.mark.gpu
 
 CASES = [
-    # workload, populated layers (None = all)
-    ("qwen_1l", None),
-    ("qwen_36l_8k", [0, 1, 2]),
-    ("batched_mixed", None),
+    # workload, populated layers (None = all), one patch of every layer then a
+    # call per layer (the bench's configuration) or a patch inside every call
+    ("qwen_1l", None, True),
+    ("qwen_36l_8k", [0, 1, 2], True),
+    ("batched_mixed", None, True),
+    ("qwen_1l", None, False),
 ]
 
 
@@ -28,8 +30,9 @@ def _say(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-@pytest.mark.parametrize("name,layers", CASES, ids=[c[0] for c in CASES])
-def test_graph_replays_match_eager(name, layers):
+@pytest.mark.parametrize("name,layers,split", CASES,
+                         ids=[c[0] + ("" if c[2] else "_patch_per_layer") for c in CASES])
+def test_graph_replays_match_eager(name, layers, split):
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     from paper_2608_21362_amd import pipeline
@@ -44,8 +47,13 @@ def test_graph_replays_match_eager(name, layers):
     def step():
         pipeline.stitch(di, pb)
         pipeline.deviation_topk(di, pb)
-        for i in range(di.n_layers):
-            pipeline.sparse_attn_layer(di, pb, i)
+        if split:
+            pipeline.patch(di, pb)
+            for i in range(di.n_layers):
+                pipeline.attn_layer(di, pb, i)
+        else:
+            for i in range(di.n_layers):
+                pipeline.sparse_attn_layer(di, pb, i)
 
     outputs = lambda: (pb.k_cache, pb.v_cache, pb.v_cache_f16, pb.delta, pb.rows,  # noqa: E731
                        pb.cu_rows, pb.out)
