@@ -573,10 +573,16 @@ __device__ __forceinline__ void attend_segment(
 }
 
 // Plan area (int32): [0] c1, [1] c2, [2] n_second, [3] total, [4 .. 4+n_tiles]
-// prefix, [5+n_tiles ..) first tile of every workgroup (by range index), then
-// the per-tile metadata (int4) at this offset.
-__host__ __device__ constexpr int64_t tile_meta_offset(int64_t n_tiles, int64_t n_wg_max) {
-  return ((5 + n_tiles + n_wg_max + 3) / 4) * 4;
+// prefix, then the per-tile metadata (int4) at tile_meta_offset, then one
+// 32-byte first-segment descriptor per workgroup at range_seg_offset.
+__host__ __device__ constexpr int64_t tile_meta_offset(int64_t n_tiles) {
+  return ((5 + n_tiles + 3) / 4) * 4;
+}
+__host__ __device__ constexpr int64_t range_seg_offset(int64_t n_tiles) {
+  return tile_meta_offset(n_tiles) + 4 * n_tiles;
+}
+__host__ __device__ constexpr int64_t plan_ints(int64_t n_tiles, int64_t n_wg_max) {
+  return range_seg_offset(n_tiles) + 8 * n_wg_max;
 }
 
 // Ranges are numbered by a range index v: the n2 second-slot workgroups take
@@ -612,9 +618,13 @@ __device__ __forceinline__ int range_of(int w, int n_first, int n2) {
 // ranges (second-slot workgroups), c1 for the others, sized to cover every unit.
 //   plan[0] = c1, plan[1] = c2, plan[2] = n2, plan[3] = total,
 //   plan[4 .. 4+n_tiles] = prefix,
-//   plan[5+n_tiles .. 5+n_tiles+n_wg) = tile holding unit unit_start(v),
-//   then per tile an int4 {first row entry, end row entry, key start, key end}
-//   at the 16-byte aligned offset tile_meta_offset(n_tiles, n_wg_max).
+//   per tile an int4 {first row entry, end row entry, key start, key end} at
+//   the 16-byte aligned offset tile_meta_offset(n_tiles),
+//   per attention workgroup w (indexed by w, not by range index, so that a
+//   workgroup fetches it together with the plan's head) two int4 at
+//   range_seg_offset(n_tiles): {t, prefix[t], prefix[t + 1], 0} and the
+//   metadata of t, where t is the tile holding the first unit of w's range
+//   (t = n_tiles for a range past the last unit).
 __device__ __forceinline__ void build_plan(
     int32_t n_tiles, int32_t tile_slots, int32_t Hkv, int64_t t_total,
     const int32_t* __restrict__ cu_seqlens, int32_t n_seqs, const int32_t* __restrict__ rows,
@@ -624,8 +634,8 @@ __device__ __forceinline__ void build_plan(
   __shared__ int carry_sh;
   __shared__ int prefix_sh[2 * kAttnMaxWorkgroups + 1];  // balanced ranges: n_tiles < 2 n_wg
   int32_t* prefix = plan + 4;
-  int32_t* first = plan + 5 + n_tiles;
-  int4* meta = reinterpret_cast<int4*>(plan + tile_meta_offset(n_tiles, n_wg_max));
+  int4* meta = reinterpret_cast<int4*>(plan + tile_meta_offset(n_tiles));
+  int4* seg = reinterpret_cast<int4*>(plan + range_seg_offset(n_tiles));
   const int nt = blockDim.x;  // a multiple of 64, at most 1024
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   if (tid == 0) carry_sh = 0;
@@ -682,20 +692,30 @@ __device__ __forceinline__ void build_plan(
     prefix_sh[n_tiles] = total;
   }
   __syncthreads();
-  // tile holding unit unit_start(v): every non-empty tile [p0, p1) writes the
-  // ranges whose first unit lies in it (one pass, no search); ranges that
-  // start past the last unit get n_tiles (they have no work)
+  // first-segment descriptors: every non-empty tile [p0, p1) writes those of
+  // the ranges whose first unit lies in it (one pass, no search); ranges that
+  // start past the last unit get tile n_tiles (they have no work).  meta[t]
+  // was stored by this same thread in the first pass.
   for (int t = tid; t < n_tiles; t += nt) {
     const int p0 = prefix_sh[t], p1 = prefix_sh[t + 1];
     if (p1 <= p0) continue;
+    const int4 mt = meta[t];
     for (int v = unit_owner(p0, c1, c2, n2); v < n_wg; ++v) {
       const int u = unit_start(v, c1, c2, n2);
       if (u >= p1) break;
-      if (u >= p0) first[v] = t;
+      if (u >= p0) {
+        const int w = v < n2 ? v + n_first : v - n2;  // inverse of range_of
+        seg[2 * w] = make_int4(t, p0, p1, 0);
+        seg[2 * w + 1] = mt;
+      }
     }
   }
   for (int v = tid; v < n_wg; v += nt)
-    if (unit_start(v, c1, c2, n2) >= total) first[v] = n_tiles;
+    if (unit_start(v, c1, c2, n2) >= total) {
+      const int w = v < n2 ? v + n_first : v - n2;
+      seg[2 * w] = make_int4(n_tiles, total, total, 0);
+      seg[2 * w + 1] = make_int4(0, 0, 0, 0);
+    }
 }
 
 // Patch: cache[l][h][t] <- fresh[l][h][t] for every selected row t (both
@@ -798,34 +818,44 @@ attn_kernel(int32_t balanced, int32_t n_tiles, int32_t Hq, int32_t Hkv, int32_t 
                       rows_per_layer, q, kc, v16, c_log2, out_f32, out, parts);
     return;
   }
+  // the plan's head and this workgroup's first-segment descriptor are
+  // independent loads: the first tile's blocks can be requested right after
   const int c1 = plan[0], c2 = plan[1], n2 = plan[2], total = plan[3];
+  const int4* sd = reinterpret_cast<const int4*>(plan + range_seg_offset(n_tiles)) + 2 * blockIdx.x;
+  const int4 s0 = sd[0];
+  int4 mt = sd[1];
   const int n_lg = n_tiles / tile_slots;
   const int v = range_of(blockIdx.x, (int)gridDim.x - n2, n2);  // range index
   const int32_t* prefix = plan + 4;
-  const int4* meta = reinterpret_cast<const int4*>(plan + tile_meta_offset(n_tiles, n_wg_max));
+  const int4* meta = reinterpret_cast<const int4*>(plan + tile_meta_offset(n_tiles));
   int u = unit_start(v, c1, c2, n2);
   const int u_end = min(unit_start(v + 1, c1, c2, n2), total);
-  int t = plan[5 + n_tiles + v];
-  for (int seg = 0; u < u_end && t < n_tiles; ++t) {
-    const int p0 = prefix[t], p1 = prefix[t + 1];
-    if (p1 <= u) continue;  // empty tile (or before the range)
-    const int e = min(u_end, p1);
-    // units [p0, p0 + kSegCost) of a tile stand for its fixed cost and hold no block
-    const int b_lo = max(u - p0 - kSegCost, 0), b_hi = max(e - p0 - kSegCost, 0);
-    if (b_hi > b_lo) {
-      const int rec = (u <= p0 + kSegCost && p1 <= u_end) ? -1 : 2 * v + (seg == 0 ? 0 : 1);
-      const int4 mt = meta[t];
-      SegTile tl;
-      tl.lg = t % n_lg;
-      tl.r_begin = mt.x;
-      tl.r_end = mt.y;
-      tl.kstart = mt.z;
-      tl.kend = mt.w;
-      attend_segment<D>(tl, b_lo, b_hi, rec, n_rec, k_ring, v_ring, Hq, Hkv, log2g, t_total, rows,
-                        rows_per_layer, q, kc, v16, c_log2, out_f32, out, parts);
-      ++seg;
+  int t = s0.x, p0 = s0.y, p1 = s0.z;
+  for (int seg = 0; u < u_end && t < n_tiles;) {
+    if (p1 > u) {  // else an empty tile
+      const int e = min(u_end, p1);
+      // units [p0, p0 + kSegCost) of a tile stand for its fixed cost and hold no block
+      const int b_lo = max(u - p0 - kSegCost, 0), b_hi = max(e - p0 - kSegCost, 0);
+      if (b_hi > b_lo) {
+        const int rec = (u <= p0 + kSegCost && p1 <= u_end) ? -1 : 2 * v + (seg == 0 ? 0 : 1);
+        SegTile tl;
+        tl.lg = t % n_lg;
+        tl.r_begin = mt.x;
+        tl.r_end = mt.y;
+        tl.kstart = mt.z;
+        tl.kend = mt.w;
+        attend_segment<D>(tl, b_lo, b_hi, rec, n_rec, k_ring, v_ring, Hq, Hkv, log2g, t_total,
+                          rows, rows_per_layer, q, kc, v16, c_log2, out_f32, out, parts);
+        ++seg;
+      }
+      u = e;
     }
-    u = e;
+    // later tiles of the range: their prefix end and metadata from the plan
+    if (++t < n_tiles && u < u_end) {
+      p0 = p1;
+      p1 = prefix[t + 1];
+      mt = meta[t];
+    }
   }
 }
 
@@ -842,7 +872,7 @@ combine_kernel(int32_t n_tiles, int32_t n_wg_max, int32_t Hq, int32_t Hkv, int32
   const int t = blockIdx.x;
   const int c1 = plan[0], c2 = plan[1], n2 = plan[2];
   const int p0 = plan[4 + t], p1 = plan[5 + t];
-  const int4 mt = reinterpret_cast<const int4*>(plan + tile_meta_offset(n_tiles, n_wg_max))[t];
+  const int4 mt = reinterpret_cast<const int4*>(plan + tile_meta_offset(n_tiles))[t];
   if (p1 <= p0) return;
   // the tile's blocks are units [p0 + kSegCost, p1), held by ranges w_a .. w_b
   const int w_a = unit_owner(p0 + kSegCost, c1, c2, n2), w_b = unit_owner(p1 - 1, c1, c2, n2);
@@ -960,14 +990,14 @@ bool attn_plan(int n_layers, int n_q_heads, int n_kv_heads, int head_dim, int64_
   plan->v16_in_ws = !v16_given;
   const size_t v16 =
       v16_given ? 0 : (size_t)n_layers * n_kv_heads * (size_t)t_total * head_dim * 2;
-  const size_t plan_ints = (size_t)tile_meta_offset(n_tiles, plan->n_wg_max) + 4 * (size_t)n_tiles;
+  const size_t n_plan_ints = (size_t)plan_ints(n_tiles, plan->n_wg_max);
   const size_t parts = (size_t)(head_dim == 128 ? rec_ml_offset<128>(plan->n_rec)
                                                  : rec_ml_offset<64>(plan->n_rec)) +
                        (size_t)plan->n_rec * kQT * 2 * sizeof(float);
   auto up = [](size_t x) { return ((x + 255) / 256) * 256; };
   plan->v16_offset = 0;
   plan->plan_offset = up(v16);
-  plan->parts_offset = up(plan->plan_offset + plan_ints * sizeof(int32_t));
+  plan->parts_offset = up(plan->plan_offset + n_plan_ints * sizeof(int32_t));
   plan->workspace = plan->parts_offset + parts;
   (void)max_seq_len;
   return true;
@@ -1072,8 +1102,7 @@ hipError_t launch_sparse_attn(const AttnPlan& plan, int n_layers, int n_q_heads,
 }
 
 size_t layer_plan_stride(const AttnPlan& layer_plan) {
-  const size_t ints = (size_t)tile_meta_offset(layer_plan.n_tiles, layer_plan.n_wg_max) +
-                      4 * (size_t)layer_plan.n_tiles;
+  const size_t ints = (size_t)plan_ints(layer_plan.n_tiles, layer_plan.n_wg_max);
   return ((ints * sizeof(int32_t) + 255) / 256) * 256;
 }
 
