@@ -58,6 +58,7 @@ struct AttnPlan {
   int n_tiles;         // layers x kv heads x tile slots
   int n_wg_max;        // most attention workgroups a launch uses
   int n_rec;           // partial records (two per workgroup)
+  int max_seq_len;     // longest prompt (bounds the key blocks of any tile)
   bool v16_in_ws;      // the fp16 copy of V lives in the workspace (no shadow given)
   size_t v16_offset;   // workspace offset of the fp16 copy of V
   size_t plan_offset;  // workspace offset of the work decomposition (int32)

@@ -999,7 +999,7 @@ bool attn_plan(int n_layers, int n_q_heads, int n_kv_heads, int head_dim, int64_
   plan->plan_offset = up(v16);
   plan->parts_offset = up(plan->plan_offset + n_plan_ints * sizeof(int32_t));
   plan->workspace = plan->parts_offset + parts;
-  (void)max_seq_len;
+  plan->max_seq_len = max_seq_len;
   return true;
 }
 
@@ -1014,9 +1014,15 @@ void launch_shape(const AttnPlan& plan, int* n_wg, int* n_first) {
   *n_wg = w;
 }
 
-// Enough tiles to keep every resident workgroup busy twice over: one tile per
-// workgroup, no partial records; otherwise balanced ranges.
-bool is_balanced(const AttnPlan& plan, int n_wg) { return plan.n_tiles < 2 * n_wg; }
+// One tile per workgroup (no partial records, no combine launch) when there
+// are enough tiles to keep every resident workgroup busy twice over, or when
+// no prompt is longer than kWholeTileMaxSeq rows: no tile then has more than
+// 16 key blocks, and a launch of short whole tiles ends sooner than balanced
+// ranges followed by the merge of their cut tiles.  Otherwise balanced ranges.
+constexpr int kWholeTileMaxSeq = 512;
+bool is_balanced(const AttnPlan& plan, int n_wg) {
+  return plan.n_tiles < 2 * n_wg && plan.max_seq_len > kWholeTileMaxSeq;
+}
 
 // Patch launch: copies the selected rows of n_layers layers; with plans != NULL
 // its first n_plans workgroups build the plans (see patch_kernel).
