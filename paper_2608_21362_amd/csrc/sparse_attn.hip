@@ -718,8 +718,10 @@ __device__ __forceinline__ void build_plan(
     }
 }
 
+constexpr int kPatchRows = 4;  // row-list entries per patch wave
+
 // Patch: cache[l][h][t] <- fresh[l][h][t] for every selected row t (both
-// tensors, every kv head; one wave per row), with the fp16 image of the new V
+// tensors, every kv head; one wave per kPatchRows rows), with the fp16 image of the new V
 // rows when the caller keeps an fp16 shadow of V.  With plan != NULL the first
 // n_plans workgroups build work decompositions instead: one plan over all L
 // layers (n_plans = 1), or one plan per layer (n_plans = L, plan p at
@@ -752,28 +754,52 @@ patch_kernel(int32_t L, int32_t Hkv, int32_t D, int64_t t_total, int32_t n_seqs,
   const int64_t copy_block = (int64_t)blockIdx.x - (plan != nullptr ? n_plans : 0);
   const int64_t wave = (copy_block * blockDim.x + threadIdx.x) >> 6;
   const int lane = threadIdx.x & 63;
-  const int64_t l = wave / max_rows;
-  const int64_t i = wave % max_rows;
+  // each wave copies kPatchRows consecutive entries of the row list, with all
+  // their loads in flight together
+  const int64_t groups = (max_rows + kPatchRows - 1) / kPatchRows;
+  const int64_t l = wave / groups;
+  const int64_t i0 = (wave % groups) * kPatchRows;
   if (l >= L) return;
   const int64_t set = rows_per_layer ? l : 0;
   const int32_t n = cu_rows[set * (n_seqs + 1) + n_seqs];
-  if (i >= n) return;
-  const int64_t t = rows[set * t_total + i];
-  if (t < 0 || t >= t_total) return;
+  if (i0 >= n) return;
+  int64_t t[kPatchRows];
+  bool ok[kPatchRows];
+#pragma unroll
+  for (int r = 0; r < kPatchRows; ++r) {
+    t[r] = rows[set * t_total + min(i0 + r, (int64_t)n - 1)];
+    ok[r] = i0 + r < n && t[r] >= 0 && t[r] < t_total;
+  }
+  // an entry that is not copied reads a valid row (loads stay unconditional)
+  int64_t t_any = -1;
+#pragma unroll
+  for (int r = kPatchRows - 1; r >= 0; --r)
+    if (ok[r]) t_any = t[r];
+  if (t_any < 0) return;
   const int chunks = D / 8;  // 16-byte pieces per head row
   for (int e = lane; e < 2 * Hkv * chunks; e += 64) {
     const int tensor = e / (Hkv * chunks);
     const int h = (e / chunks) % Hkv;
     const int c = e % chunks;
-    const int64_t off = (((l * Hkv + h) * t_total) + t) * D + c * 8;
-    if (tensor == 0) {
-      *reinterpret_cast<uint4*>(kc + off) = *reinterpret_cast<const uint4*>(kf + off);
-    } else {
-      const uint4 a = *reinterpret_cast<const uint4*>(vf + off);
-      *reinterpret_cast<uint4*>(vc + off) = a;
-      if (vh)
-        *reinterpret_cast<uint4*>(vh + off) = make_uint4(bf16x2_to_f16x2(a.x), bf16x2_to_f16x2(a.y),
-                                                         bf16x2_to_f16x2(a.z), bf16x2_to_f16x2(a.w));
+    const int64_t base = (l * Hkv + h) * t_total;
+    const uint16_t* src = tensor == 0 ? kf : vf;
+    uint4 a[kPatchRows];
+#pragma unroll
+    for (int r = 0; r < kPatchRows; ++r)
+      a[r] = *reinterpret_cast<const uint4*>(src + (base + (ok[r] ? t[r] : t_any)) * D + c * 8);
+#pragma unroll
+    for (int r = 0; r < kPatchRows; ++r) {
+      if (!ok[r]) continue;
+      const int64_t off = (base + t[r]) * D + c * 8;
+      if (tensor == 0) {
+        *reinterpret_cast<uint4*>(kc + off) = a[r];
+      } else {
+        *reinterpret_cast<uint4*>(vc + off) = a[r];
+        if (vh)
+          *reinterpret_cast<uint4*>(vh + off) =
+              make_uint4(bf16x2_to_f16x2(a[r].x), bf16x2_to_f16x2(a[r].y),
+                         bf16x2_to_f16x2(a[r].z), bf16x2_to_f16x2(a[r].w));
+      }
     }
   }
 }
@@ -1032,7 +1058,7 @@ void launch_patch(int n_layers, int n_kv_heads, int head_dim, int64_t t_total,
                   const uint16_t* k_fresh, const uint16_t* v_fresh, uint16_t* k_cache,
                   uint16_t* v_cache, uint16_t* v_f16, const AttnPlan& plan, int n_wg, int n_first,
                   int32_t* plans, int n_plans, int64_t plan_stride, hipStream_t s) {
-  const int64_t waves = (int64_t)n_layers * max_rows;
+  const int64_t waves = (int64_t)n_layers * ((max_rows + kPatchRows - 1) / kPatchRows);
   const int64_t blocks = (waves * 64 + 255) / 256 + (plans ? n_plans : 0);
   if (blocks > 0)
     hipLaunchKernelGGL(patch_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n_layers, n_kv_heads,
