@@ -88,11 +88,13 @@ constexpr int kAttnMaxWorkgroups = 1024;  // attention workgroups (sizes the par
 constexpr int kSegCost = 7;
 // With two workgroups per CU the dispatcher gives workgroups 0 .. CUs-1 the
 // first slot of every CU and the rest the second; the hardware issues the
-// older (first) workgroup's waves first, so it progresses about 1.4 times
-// faster while both run.  Balanced ranges give first-slot workgroups 7/5 of the
-// units of second-slot ones so that the two finish together (measured; a
-// different placement only costs balance, never correctness).
-constexpr int kFirstShareNum = 7, kFirstShareDen = 5;
+// older (first) workgroup's waves first, so it progresses faster while both
+// run (about 1.2 to 1.4 times per block in timestamped runs).  Balanced ranges
+// give first-slot workgroups 8/5 of the units of second-slot ones so that the
+// two finish together (measured on MI355X at 8K keys per prompt: 8/5 and 3/2
+// gave the shortest launches, 7/5 and 13/10 about 1 % longer; a different
+// placement only costs balance, never correctness).
+constexpr int kFirstShareNum = 8, kFirstShareDen = 5;
 constexpr float kLazy = 8.0f;           // max growth (log2 units) tolerated before a rescale
 
 #define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
