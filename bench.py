@@ -1,19 +1,28 @@
 """Benchmark of the stitched-prefill path on one MI355X.
 
-One step = one pass of the whole path over one 8K-token prompt of the
-36-layer Qwen2.5-3B-shaped workload (16 query / 2 KV heads, d = 128, int4
-KIVI pool with 64 cached chunks at random original offsets, 15 % per-layer
-recompute):
+One step = one pass of the whole path over one batch of a workload, by
+default one 8K-token prompt of the 36-layer Qwen2.5-3B-shaped workload
+(16 query / 2 KV heads, d = 128, int4 KIVI pool with 64 cached chunks at
+random original offsets, 15 % per-layer recompute):
 
-    kvb_stitch (all layers, one launch; also keeps the fp16 shadow of V)
-    kvb_deviation_topk (all layers, one call: deviation + selection)
-    kvb_sparse_attn x 36 (one call per layer, as a model runs its layers)
+    kvb_stitch_deviation (all layers, one launch: dequantise + re-rotate the
+                          cached chunks, keep the fp16 shadow of V, and the
+                          per-layer K deviation of the stitched rows)
+    kvb_select           (all layers, one launch)
+    kvb_patch            (all layers, one launch; also the attention plans)
+    kvb_sparse_attn_layer x 36 (one call per layer, as a model runs its layers)
 
-Inputs are resident in HBM before the timed region.  Prints one JSON line.
-The roofline object covers the per-layer attention call (the dominant cost):
-algorithmic flops per call / its average duration from HIP events on the
-stream it runs on; "traffic" is the per-call HBM bytes from the committed
-rocprofv3 counter summary when it was taken on the current kernel sources.
+captured once in a HIP graph and replayed.  Inputs are resident in HBM before
+the timed region.  Prints one JSON line.
+
+``roofline`` covers the dominant call, the per-layer attention: algorithmic
+flops per call / its average duration from HIP events on the stream it runs
+on; "traffic" is the per-call HBM bytes from the committed rocprofv3 counter
+summary when it was taken on the current kernel sources.  ``rooflines`` adds
+the same figures for the bandwidth-bound calls (stitch, deviation, fused
+stitch + deviation) on the method's own bytes, timed with the Infinity Cache
+flushed; the fp16 shadow of V that the stitch also writes (the attention's
+P.V operand, not part of the method) is reported as an overhead next to them.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--attn-all-layers] [--no-cpu-baseline]
@@ -40,34 +49,42 @@ def log(*a):
 
 
 def algorithmic(w, s, rows_per_set, cu_rows_per_set):
-    """Algorithmic work of one step (bytes a kernel must move, flops it must do).
+    """Algorithmic work of one step: the bytes each bandwidth-bound call must
+    move for the method itself, and the attention's flops.
 
-    Stitch: the codes and statistics it reads, the bf16 K and V rows it writes
-    and the fp16 shadow of V it keeps for the attention.  Deviation: the cache
-    and fresh K rows it reads (bf16) and the deviation it writes.  Fused stitch +
-    deviation: the stitch's bytes plus the fresh K rows of the stitched chunks
-    and their deviations.  Attention: 4 d Hq flops per (selected query row,
-    visible key): QK^T and PV."""
+    Stitch (Eq. 7 dequantisation and the Sec. 3.2 re-rotation): the codes and
+    statistics it reads and the bf16 K and V rows it writes.  Deviation (Alg. 2
+    step 2): the stitched and fresh K rows it reads (bf16) and the deviation it
+    writes.  Fused stitch + deviation: the stitch's bytes plus the fresh K rows
+    of the stitched chunks and their deviations.  The fp16 shadow of V, which
+    the stitch also writes for the attention's P.V operand, is not the
+    method's work: its bytes are returned separately.  Attention (Eq. 2):
+    4 d Hq flops per (selected query row, visible key): QK^T and PV."""
     L, H, d, C, T, Hq = w.n_layers, w.n_kv_heads, w.head_dim, w.chunk_len, w.t_total, w.n_q_heads
     P = s.n_pool
     cb = d * w.bits // 8
     codes = 2 * P * L * H * C * cb
     stats = P * L * H * (C // w.k_group) * d * 8 + P * L * H * C * (d // w.v_group) * 8
-    stitch_out = 3 * P * L * H * C * d * 2
-    stitch_bytes = codes + stats + stitch_out
+    stitch_out = 2 * P * L * H * C * d * 2
+    shadow = P * L * H * C * d * 2
     n_sets = rows_per_set.shape[0]
-    dev_bytes = 2 * L * H * T * d * 2 + n_sets * T * 4
-    fused_bytes = stitch_bytes + P * L * H * C * d * 2 + L * P * C * 4
+    fresh_k = P * L * H * C * d * 2
+    b = {
+        "stitch": codes + stats + stitch_out,
+        "deviation": 2 * L * H * T * d * 2 + n_sets * T * 4,
+        "stitch_deviation": codes + stats + stitch_out + fresh_k + L * P * C * 4,
+        "shadow": shadow,
+    }
     # bytes read of each (the rest is written), for the practical ceilings
-    algorithmic.reads = {"stitch": codes + stats, "deviation": 2 * L * H * T * d * 2,
-                         "stitch_deviation": codes + stats + P * L * H * C * d * 2}
+    reads = {"stitch": codes + stats, "deviation": 2 * L * H * T * d * 2,
+             "stitch_deviation": codes + stats + fresh_k}
     pos = s.positions().astype(np.int64)
     flops_per_layer = []
     for l in range(L):
         si = l if w.per_layer else 0
         r = rows_per_set[si, : cu_rows_per_set[si, -1]]
         flops_per_layer.append(4.0 * d * Hq * float(np.sum(pos[r] + 1)))
-    return stitch_bytes, dev_bytes, fused_bytes, np.array(flops_per_layer)
+    return b, reads, np.array(flops_per_layer)
 
 
 def committed_traffic(workload, key="traffic_bytes_per_launch"):
@@ -99,9 +116,29 @@ def committed_traffic(workload, key="traffic_bytes_per_launch"):
 KERNEL_SOURCES = ("paper_2608_21362_amd/csrc/sparse_attn.hip", "paper_2608_21362_amd/csrc/kvb_device.h")
 
 
-def cpu_baseline(w, s, n_layers_sample):
-    """The oracle as it stands, on the first ``n_layers_sample`` layers of the
-    same workload; scaled to the whole step linearly in layers."""
+def cpu_host():
+    """The host the oracle runs on: core count, CPU model, OMP_NUM_THREADS."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"os_cpu_count": os.cpu_count(), "cpu_model": model,
+            "OMP_NUM_THREADS": os.environ.get("OMP_NUM_THREADS")}
+
+
+def cpu_baseline(w, s, n_layers_sample, attn_rows_sample=0):
+    """The oracle as it stands on the first ``n_layers_sample`` layers of the
+    same workload, stage by stage (stitch; deviation + selection; patch +
+    attention), scaled to the whole step linearly in layers.  With
+    ``attn_rows_sample`` > 0 the attention is evaluated on that many selected
+    rows per layer, spread evenly over the set (rows are independent), and
+    scaled by the ratio of visible keys (sum of pi(t) + 1) over all selected
+    rows to that over the sample; such a figure is labelled extrapolated."""
     from threadpoolctl import threadpool_info
 
     from oracle import path as opath
@@ -109,18 +146,41 @@ def cpu_baseline(w, s, n_layers_sample):
 
     layers = list(range(n_layers_sample))
     pop = opop.populate(w, s, layers=layers)
+    pos = s.positions().astype(np.int64)
+    work = {}
+
+    def sampler(i, sel):
+        sel = np.asarray(sel)
+        pick = sel
+        if attn_rows_sample and len(sel) > attn_rows_sample:
+            pick = sel[np.linspace(0, len(sel) - 1, attn_rows_sample).astype(np.int64)]
+        work[i] = (float(np.sum(pos[sel] + 1)), float(np.sum(pos[pick] + 1)))
+        return pick
+
+    tm = {}
     t0 = time.perf_counter()
-    opath.run(w, s, pop)
+    opath.run(w, s, pop, attend_rows=sampler, timings=tm)
     dt = time.perf_counter() - t0
-    per_step = dt / n_layers_sample * w.n_layers
+    scale = w.n_layers / n_layers_sample
+    attn_ratio = (sum(a for a, _ in work.values()) / sum(b for _, b in work.values())
+                  if work else 1.0)
+    stages = {"stitch_s": tm["stitch"] * scale,
+              "deviation_select_s": tm["deviation_select"] * scale,
+              "patch_attention_s": tm["patch_attention"] * scale * attn_ratio}
+    per_step = sum(stages.values())
     blas = [i.get("num_threads", 1) for i in threadpool_info()]
+    extrapolated = attn_ratio > 1.0
+    sample = (f"{n_layers_sample} of {w.n_layers} layers, stitch, deviation, selection and "
+              f"patch in full, attention on "
+              + (f"{attn_rows_sample} evenly spread selected rows per layer (scaled by visible "
+                 f"keys x{attn_ratio:.1f}: extrapolated)" if extrapolated
+                 else "every selected row")
+              + f"; {dt:.1f} s of CPU time; scaled to {w.n_layers} layers")
     return {
         "value": w.t_total / per_step, "unit": "tokens/s",
         "cores": int(max(blas) if blas else 1), "kind": "oracle",
-        "sample": f"{n_layers_sample} of {w.n_layers} layers, every selected row "
-                  f"(stitch, deviation, selection, patch, attention), {dt:.1f} s of CPU time; "
-                  f"scaled to {w.n_layers} layers",
-        "seconds": dt,
+        "sample": sample, "seconds": dt, "stages_per_step": stages,
+        "attention_extrapolated": extrapolated, "host": cpu_host(),
     }
 
 
@@ -207,6 +267,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=24,
                     help="layers of the oracle timed for cpu_baseline (scaled to the whole step)")
+    ap.add_argument("--cpu-attn-rows", type=int, default=0,
+                    help="evaluate the oracle's attention on this many selected rows per layer "
+                         "and scale by visible keys (0: every selected row)")
     ap.add_argument("--flush-mb", type=int, default=512)
     ap.add_argument("--calibrate-copy-mb", type=int, default=0,
                     help="also run one plain device copy of this size (counter calibration)")
@@ -329,7 +392,7 @@ def main():
 
     rows = pb.rows.cpu().numpy()
     cu = pb.cu_rows.cpu().numpy()
-    st_bytes, dev_bytes, sd_bytes, flops = algorithmic(w, s, rows, cu)
+    nbytes, nreads, flops = algorithmic(w, s, rows, cu)
     attn_flops_launch = float(flops.mean()) if not args.attn_all_layers else float(flops.sum())
     attn_tflops = attn_flops_launch / (attn_ms_launch * 1e-3) / 1e12
 
@@ -338,22 +401,26 @@ def main():
     # timed call neither hits its inputs in the cache nor pays for another
     # kernel's write-back
     flush = torch.ones(args.flush_mb << 18, dtype=torch.float32, device="cuda")
-    st_f, dv_f, d_f, sd_f = [], [], [], []
+    flushed = {"stitch": [], "stitch_no_shadow": [], "deviation_topk": [], "deviation": [],
+               "stitch_deviation": []}
+    calls = {"stitch": lambda: pipeline.stitch(di, pb),
+             "stitch_no_shadow": lambda: pipeline.stitch(di, pb, shadow=False),
+             "deviation_topk": lambda: pipeline.deviation_topk(di, pb),
+             "deviation": lambda: pipeline.deviation(di, pb),
+             "stitch_deviation": lambda: pipeline.stitch_deviation(di, pb)}
     for _ in range(5):
         # flush, then the timed call right behind it on the same stream (no
         # host synchronisation in between, so the interval holds no idle
         # launch latency)
-        for fn, acc in ((lambda: pipeline.stitch(di, pb), st_f),
-                        (lambda: pipeline.deviation_topk(di, pb), dv_f),
-                        (lambda: pipeline.deviation(di, pb), d_f),
-                        (lambda: pipeline.stitch_deviation(di, pb), sd_f)):
+        for name, fn in calls.items():
             flush.sum()
             a, b = ev(), ev()
             a.record(stream)
             fn()
             b.record(stream)
             torch.cuda.synchronize()
-            acc.append(a.elapsed_time(b))
+            flushed[name].append(a.elapsed_time(b))
+    fl_ms = {k: float(np.median(v)) for k, v in flushed.items()}
     # chunk importance (cache population, Sec. 4.4; not part of the step): fp32
     # keys of every pool chunk and layer, cache flushed before each repetition
     from paper_2608_21362_amd import kvb as _kvb
@@ -374,10 +441,6 @@ def main():
     imp_gbs = imp_bytes / (np.median(imp_f) * 1e-3) / 1e9
     del k_pool, imp
     del flush
-    st_gbs = st_bytes / (np.median(st_f) * 1e-3) / 1e9
-    dv_gbs = dev_bytes / (np.median(dv_f) * 1e-3) / 1e9
-    d_gbs = dev_bytes / (np.median(d_f) * 1e-3) / 1e9
-    sd_gbs = sd_bytes / (np.median(sd_f) * 1e-3) / 1e9
 
     log("[bench] practical ceilings")
     ceil = measure_ceilings(torch)
@@ -393,6 +456,36 @@ def main():
         (None, "") if args.attn_all_layers else
         committed_traffic(w.name, "traffic_bytes_per_launch" if patch_once
                           else "traffic_bytes_per_launch_with_patch"))
+    def bw(name, key):
+        """Roofline figures of a bandwidth-bound call on the method's bytes (and,
+        next to them, on every byte it moves, the fp16 shadow of V included)."""
+        by = nbytes[key]
+        ms = fl_ms[name]
+        gbs = by / (ms * 1e-3) / 1e9
+        total = nbytes[key] + (nbytes["shadow"] if key in ("stitch", "stitch_deviation") and
+                               name != "stitch_no_shadow" else 0)
+        r = {"bound": "hbm", "bytes": int(by), "us": ms * 1e3, "achieved": gbs,
+             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
+             "bytes_moved_incl_overhead": int(total),
+             "GBps_incl_overhead": total / (ms * 1e-3) / 1e9,
+             "frac_of_practical": practical_frac(total / (ms * 1e-3) / 1e9, total,
+                                                 nreads[key], ceil),
+             "timing": "median of 5 flushed calls (HIP events)"}
+        return r
+
+    rooflines = {
+        "stitch": bw("stitch", "stitch"),
+        "deviation": bw("deviation", "deviation"),
+        "stitch_deviation": bw("stitch_deviation", "stitch_deviation"),
+        "stitch_without_shadow": bw("stitch_no_shadow", "stitch"),
+    }
+    shadow_overhead = {
+        "bytes": int(nbytes["shadow"]),
+        "what": "fp16 image of every stitched V row (the attention's P.V operand); written "
+                "by the stitch next to the method's bf16 cache",
+        "stitch_us_with": fl_ms["stitch"] * 1e3, "stitch_us_without": fl_ms["stitch_no_shadow"] * 1e3,
+        "us": (fl_ms["stitch"] - fl_ms["stitch_no_shadow"]) * 1e3,
+    }
     tokens_per_step = w.t_total
     result = {
         "metric": METRIC,
@@ -434,6 +527,8 @@ def main():
             "timing": "HIP events around each call in eager steps",
             "frac_of_measured_ceiling": attn_tflops / ceil["mfma_bf16_TFLOPs"],
         },
+        "rooflines": rooflines,
+        "shadow_overhead": shadow_overhead,
         "ceilings": ceil,
         "kernels": {
             "ms_per_step_eager": ms_step_eager, "ms_per_step_graph": ms_step_graph,
@@ -441,31 +536,21 @@ def main():
             ("select_ms" if fused else "deviation_topk_ms"): float(dv_ms),
             "patch_ms": pt_ms,
             "sparse_attn_ms_per_step": float(at_ms.sum(axis=1).mean()),
-            "stitch_GBps_flushed": st_gbs, "stitch_hbm_frac": st_gbs / HBM_PEAK_GBS,
-            "stitch_bytes": st_bytes,
-            "deviation_GBps_flushed": d_gbs, "deviation_hbm_frac": d_gbs / HBM_PEAK_GBS,
-            "deviation_topk_GBps_flushed": dv_gbs, "deviation_topk_hbm_frac": dv_gbs / HBM_PEAK_GBS,
-            "select_ms_flushed": float(np.median(dv_f) - np.median(d_f)),
-            "stitch_deviation_GBps_flushed": sd_gbs, "stitch_deviation_hbm_frac": sd_gbs / HBM_PEAK_GBS,
-            "stitch_deviation_bytes": sd_bytes,
-            "deviation_bytes": dev_bytes,
+            "deviation_topk_ms_flushed": fl_ms["deviation_topk"],
+            "select_ms_flushed": fl_ms["deviation_topk"] - fl_ms["deviation"],
             "chunk_importance_GBps_flushed": imp_gbs,
             "chunk_importance_hbm_frac": imp_gbs / HBM_PEAK_GBS,
             "chunk_importance_bytes": int(imp_bytes),
-            "selected_rows_per_layer": float(np.mean(cu[:, -1])),
-            "stitch_frac_of_practical": practical_frac(st_gbs, st_bytes,
-                                                       algorithmic.reads["stitch"], ceil),
-            "deviation_frac_of_practical": practical_frac(d_gbs, dev_bytes,
-                                                          algorithmic.reads["deviation"], ceil),
-            "stitch_deviation_frac_of_practical": practical_frac(
-                sd_gbs, sd_bytes, algorithmic.reads["stitch_deviation"], ceil),
             "chunk_importance_frac_of_practical": practical_frac(
                 imp_gbs, imp_bytes, imp_bytes - P * 8, ceil),
+            "selected_rows_per_layer": float(np.mean(cu[:, -1])),
         },
     }
     if not args.no_cpu_baseline:
-        log(f"[bench] cpu baseline: oracle on {args.cpu_layers} layers")
-        result["cpu_baseline"] = cpu_baseline(w, s, args.cpu_layers)
+        n_cpu = min(args.cpu_layers, w.n_layers)
+        log(f"[bench] cpu baseline: oracle on {n_cpu} layers"
+            + (f", attention on {args.cpu_attn_rows} rows per layer" if args.cpu_attn_rows else ""))
+        result["cpu_baseline"] = cpu_baseline(w, s, n_cpu, args.cpu_attn_rows)
     print(json.dumps(result), flush=True)
 
 

@@ -23,7 +23,7 @@
  * plus the host helpers that prepare their inputs (rotation tables, row
  * flags, the threshold-activated probe of Sec. 7.4) and the cache-population
  * kernels (RoPE at absolute positions, KIVI quantisation, chunk importance;
- * Sec. 4.6 warm, Sec. 4.4).
+ * Sec. 4.7 warm, Sec. 4.4).
  *
  * Conventions
  *   - Every pointer named as a tensor, descriptor, index or workspace is a
@@ -150,7 +150,7 @@ kvb_status kvb_probe_gate(int32_t n_seqs, const int32_t* cu_seqlens, const uint8
                           int32_t min_num, int32_t min_den, int32_t* k_per_seq,
                           int32_t* n_probed);
 
-/* ---- cache population (Sec. 4.6 warm, Sec. 4.5, Eq. 3) ----------------- */
+/* ---- cache population (Sec. 4.7 warm, Sec. 4.5, Eq. 3) ----------------- */
 
 /* RoPE at absolute positions (Eq. 3) and storage conversion.
  * x: f32 [n_outer][n_rows][n_inner][head_dim]; vector (o, r, i) is rotated by

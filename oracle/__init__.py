@@ -12,7 +12,7 @@ computes, in float64 numpy, written from the paper (KVBoost, arXiv 2608.21362):
 * ``deviation``  -- CacheBlendRecompute step 2 (Alg. 2)
 * ``selection``  -- CacheBlendRecompute step 3 (Alg. 2) united with the
                     SelectiveRecompute seam windows (Alg. 1) and live rows
-                    (Sec. 4.1 attention sinks, Sec. 4.6 live tokens)
+                    (Sec. 4.1 attention sinks, Sec. 4.7 live tokens)
 * ``attention``  -- CacheBlendRecompute step 4 patch (Alg. 2) and causal
                     attention of the selected query rows (Sec. 3.1, Eq. 2)
 * ``populate``   -- turns the seeded raw draws of ``kvb_workload`` into the

@@ -10,7 +10,7 @@
 Readings: grouped-query attention maps query head h to kv head
 floor(h * Hkv / Hq); queries are already rotated at their positions; only the
 selected rows are computed (the forward on live / recomputed tokens of
-Sec. 4.6); the cache read is the patched one.  Arithmetic is float64 over the
+Sec. 4.7); the cache read is the patched one.  Arithmetic is float64 over the
 exact float64 images of the bfloat16 inputs; softmax subtracts the row maximum.
 """
 import numpy as np

@@ -4,6 +4,7 @@ stitch (Sec. 4.3 / 3.2 / 4.5) -> deviation (Alg. 2 step 2) -> selection
 (Alg. 2 step 3, Alg. 1 windows, live rows) -> patch (Alg. 2 step 4) ->
 attention of the selected rows (Eq. 2).
 """
+import time
 from dataclasses import dataclass
 
 import numpy as np
@@ -29,12 +30,17 @@ def selection_inputs(w, s):
     return candidate, forced, k
 
 
-def run(w, s, pop, attend_layers=None, attend_rows=None) -> PathResult:
+def run(w, s, pop, attend_layers=None, attend_rows=None, timings=None) -> PathResult:
     """``attend_rows``: optional callable(layer_index, selected_rows) -> the
     subset of rows to evaluate attention on (rows are independent, so a
-    subset is exact for the rows it holds)."""
+    subset is exact for the rows it holds).  ``timings``: optional dict that
+    receives the wall time in seconds of each stage ("stitch",
+    "deviation_select", "patch_attention")."""
+    clock = time.perf_counter
+    t0 = clock()
     ck, cv = pop.cache_k.copy(), pop.cache_v.copy()
     stitch.stitch_into(ck, cv, pop.pool, pop.chunks, pop.cos, pop.sin, "bf16")
+    t1 = clock()
     delta = deviation.deviation(ck, pop.k_fresh, per_layer=w.per_layer)
     d32 = delta.astype(np.float32)
     candidate, forced, k = selection_inputs(w, s)
@@ -43,6 +49,7 @@ def run(w, s, pop, attend_layers=None, attend_rows=None) -> PathResult:
         r, cu = selection.select(d32[si], candidate, forced, s.cu_seqlens, k)
         rows.append(r)
         cus.append(cu)
+    t2 = clock()
     out, out_rows = {}, {}
     Lp = ck.shape[0]
     layers = range(Lp) if attend_layers is None else attend_layers
@@ -53,5 +60,8 @@ def run(w, s, pop, attend_layers=None, attend_rows=None) -> PathResult:
         ev = sel if attend_rows is None else attend_rows(i, sel)
         out[i] = attention.attend_rows(pop.q[i], kp, vp, ev, s.cu_seqlens)
         out_rows[i] = np.asarray(ev, dtype=np.int32)
+    t3 = clock()
+    if timings is not None:
+        timings.update(stitch=t1 - t0, deviation_select=t2 - t1, patch_attention=t3 - t2)
     return PathResult(cache_k=ck, cache_v=cv, delta=delta, rows=rows, cu_rows=cus,
                       out=out, out_rows=out_rows)

@@ -1,6 +1,6 @@
 """Oracle-side preparation of the path's inputs from the seeded raw draws.
 
-This is the cache-population side of the method (paper Sec. 4.6 ``warm``:
+This is the cache-population side of the method (paper Sec. 4.7 ``warm``:
 forward pass, KV sliced per chunk, quantised per Sec. 4.5) and the model's own
 RoPE (Eq. 3), written here independently of the HIP library:
 

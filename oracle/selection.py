@@ -112,8 +112,14 @@ def select(delta32, candidate, forced, cu_seqlens, k_per_seq):
 
 
 def kth_margin(delta32, candidate, cu_seqlens, k_per_seq):
-    """Per prompt: |delta_(k) - delta_(k+1)| of the candidate ranking (inf
-    when k is 0 or every candidate is taken)."""
+    """Per prompt: |delta_(k) - delta_(k+1)| of the candidate ranking, i.e. how
+    far the cut of the top-k lies from the next candidate.
+
+    inf when k is 0 or every candidate is taken (there is no cut to move).
+    The ordering rule decides cuts the subtraction cannot measure: a cut
+    between a number and NaN (NaN ranks below every number) is as wide as it
+    gets (inf); two equal values -- -0 and +0, or the same infinity -- are a
+    tie (0), settled by row order alone."""
     out = []
     for b in range(len(cu_seqlens) - 1):
         lo, hi = int(cu_seqlens[b]), int(cu_seqlens[b + 1])
@@ -122,6 +128,12 @@ def kth_margin(delta32, candidate, cu_seqlens, k_per_seq):
         k = int(k_per_seq[b])
         if k == 0 or k >= len(order):
             out.append(math.inf)
+            continue
+        a, c = float(delta32[order[k - 1]]), float(delta32[order[k]])
+        if math.isnan(a) or math.isnan(c):
+            out.append(0.0 if (math.isnan(a) and math.isnan(c)) else math.inf)
+        elif a == c:
+            out.append(0.0)
         else:
-            out.append(abs(float(delta32[order[k - 1]]) - float(delta32[order[k]])))
+            out.append(abs(a - c))
     return np.asarray(out)

@@ -223,15 +223,25 @@ stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
     }
   }  // heads
   if constexpr (DEV) {
-    // one lane per token quad: delta[l][dst_row + 4q .. + 3]
+    // one lane per token quad: delta[l][dst_row + 4q .. + 3], one 16-byte
+    // store when the quad is 16-byte aligned (dst_row and t_total multiples
+    // of 4), else four 4-byte stores (e.g. after one to three sink rows)
     const int job = threadIdx.x;
     if (job < KJOBS && job % TPT == 0) {
       const int q = job / TPT;
       const double n = (double)Hkv;
-      float* dp = delta + (int64_t)blockIdx.y * t_total + ch.dst_row + 4 * q;
-      *reinterpret_cast<float4*>(dp) =
-          make_float4((float)(1.0 - cos_sum[0] / n), (float)(1.0 - cos_sum[1] / n),
-                      (float)(1.0 - cos_sum[2] / n), (float)(1.0 - cos_sum[3] / n));
+      const int64_t first = (int64_t)blockIdx.y * t_total + ch.dst_row;
+      float* dp = delta + first + 4 * q;
+      const float4 dv = make_float4((float)(1.0 - cos_sum[0] / n), (float)(1.0 - cos_sum[1] / n),
+                                    (float)(1.0 - cos_sum[2] / n), (float)(1.0 - cos_sum[3] / n));
+      if ((first & 3) == 0) {
+        *reinterpret_cast<float4*>(dp) = dv;
+      } else {
+        dp[0] = dv.x;
+        dp[1] = dv.y;
+        dp[2] = dv.z;
+        dp[3] = dv.w;
+      }
     }
   }
 }

@@ -4,7 +4,11 @@ Builds the path's inputs in HBM from the seeded raw draws of ``kvb_workload``
 with the library's own population kernels (RoPE at absolute positions, KIVI
 quantisation), then runs the path through the C ABI:
 
-    kvb_stitch -> kvb_deviation_topk -> kvb_sparse_attn (per layer, or all layers at once)
+    kvb_stitch_deviation (or kvb_stitch, then kvb_deviation_topk)
+      -> kvb_select -> kvb_patch (every layer) -> kvb_sparse_attn_layer (per layer)
+
+(``run_path`` can also attend all layers in one kvb_sparse_attn call, or patch
+inside a kvb_sparse_attn call per layer.)
 
 torch provides device memory, copies and the stream; every step of the path
 runs in libkvb's HIP kernels.
@@ -70,13 +74,16 @@ class DeviceInputs:
 
 
 def populate(w: kw.Workload, s: kw.Structure, layers=None, with_q=True, draws_fn=None,
-             progress=None) -> DeviceInputs:
+             progress=None, q_layers=None) -> DeviceInputs:
     """Upload the raw draws and build pool / fresh tensors on the GPU.
-    ``progress(i, n)``, if given, is called after each populated layer."""
+    ``progress(i, n)``, if given, is called after each populated layer.
+    ``q_layers`` (layer ids), if given, limits the query draws to those layers;
+    the queries of the other layers are zero (their attention still runs, on
+    uniform scores)."""
     layers = list(range(w.n_layers)) if layers is None else list(layers)
     if draws_fn is None:
         def draws_fn(l):
-            return kw.layer_draws(w, s, l, with_q=with_q)
+            return kw.layer_draws(w, s, l, with_q=with_q and (q_layers is None or l in q_layers))
     L, H, C, d, T, Hq = len(layers), w.n_kv_heads, w.chunk_len, w.head_dim, w.t_total, w.n_q_heads
     P = s.n_pool
     pool = kvb.pool_layout(L, H, d, w.bits, w.k_group, w.v_group, C)
@@ -90,7 +97,9 @@ def populate(w: kw.Workload, s: kw.Structure, layers=None, with_q=True, draws_fn
     v_zero = torch.zeros_like(v_scale)
     k_fresh = torch.empty((L, H, T, d), dtype=torch.int16, **dev)
     v_fresh = torch.empty_like(k_fresh)
-    q = torch.empty((L, T, Hq, d), dtype=torch.int16, **dev) if with_q else None
+    q = None
+    if with_q:
+        q = (torch.empty if q_layers is None else torch.zeros)((L, T, Hq, d), dtype=torch.int16, **dev)
 
     pos = s.positions()
     max_pos = int(max(int(pos.max()) + 1, (int(s.src_pos.max()) + C) if P else 0))
@@ -116,7 +125,7 @@ def populate(w: kw.Workload, s: kw.Structure, layers=None, with_q=True, draws_fn
                           k_fresh[i])
         vr = _dev(dr.v_raw)
         kvb.kvb_rope_rows(d, H, T, 1, vr, None, None, None, None, 0, kvb.KVB_BF16, v_fresh[i])
-        if with_q:
+        if with_q and dr.q_raw is not None:
             qr = _dev(dr.q_raw)
             kvb.kvb_rope_rows(d, 1, T, Hq, qr, pos_d, None, tab_c, tab_s, max_pos, kvb.KVB_BF16,
                               q[i])
@@ -204,8 +213,10 @@ def buffers(di: DeviceInputs, out_dtype=kvb.KVB_BF16, attn_all_layers=False) -> 
 
 
 def stitch(di: DeviceInputs, pb: PathBuffers, out_dtype=kvb.KVB_BF16, k_out=None, v_out=None,
-           stream=None):
-    own = k_out is None and v_out is None and out_dtype == kvb.KVB_BF16
+           stream=None, shadow=True):
+    """Stitch into pb's bf16 cache (and its fp16 shadow of V unless ``shadow``
+    is False), or into ``k_out`` / ``v_out`` of ``out_dtype`` (no shadow)."""
+    own = k_out is None and v_out is None and out_dtype == kvb.KVB_BF16 and shadow
     kvb.kvb_stitch(di.pool, di.n_pool, di.k_codes, di.k_scale, di.k_zero, di.v_codes, di.v_scale,
                    di.v_zero, di.chunks, di.n_pool, di.rope_cos, di.rope_sin, di.w.t_total,
                    out_dtype, pb.k_cache if k_out is None else k_out,

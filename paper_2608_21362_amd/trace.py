@@ -74,6 +74,43 @@ def make_requests(n, seed):
     return out
 
 
+def request_workload(i, chunks, hits, seed, n_layers=36, probe_min_pct=0):
+    """The workload of request ``i`` of a trace drawn with ``seed``: one prompt
+    of ``chunks`` chunks whose first ``hits`` were cached."""
+    import kvb_workload as kw
+
+    return kw.Workload(
+        name=f"request{i}", n_layers=n_layers, n_q_heads=16, n_kv_heads=2, head_dim=128,
+        rope_theta=1e6, bits=4, k_group=32, v_group=32, n_prompts=1,
+        chunks_per_prompt=chunks, placement="prefix_hits", hit_chunks=hits,
+        seam_left=16, seam_right=16, probe_min_num=probe_min_pct, probe_min_den=100,
+        seed=seed * 100003 + i)
+
+
+def request_draws(w, s):
+    """A request's values: one layer's seeded draw, reused for every layer."""
+    import kvb_workload as kw
+
+    draw = kw.layer_draws(w, s, 0)
+    return lambda l: draw
+
+
+def request_calls(di, pb):
+    """The calls one request makes: the fused stitch + deviation when anything
+    is cached and probed (the stitch alone when nothing is probed), the
+    selection, the patch of every layer, then one attention call per layer."""
+    from paper_2608_21362_amd import pipeline
+
+    if di.n_pool and di.n_probed:
+        pipeline.stitch_deviation(di, pb)
+    elif di.n_pool:
+        pipeline.stitch(di, pb)
+    pipeline.select(di, pb)
+    pipeline.patch(di, pb)
+    for li in range(di.n_layers):
+        pipeline.attn_layer(di, pb, li)
+
+
 def run(n_requests=40, seed=0, n_layers=36, probe_min_pct=0, log=print):
     """Run the trace; ``probe_min_pct`` > 0 turns on the threshold-activated
     probe (Sec. 7.4): a request with fewer cached rows than that percentage
@@ -87,26 +124,13 @@ def run(n_requests=40, seed=0, n_layers=36, probe_min_pct=0, log=print):
     stream = torch.cuda.current_stream()
     results = []
     for i, (label, chunks, hits) in enumerate(make_requests(n_requests, seed)):
-        w = kw.Workload(
-            name=f"request{i}", n_layers=n_layers, n_q_heads=16, n_kv_heads=2, head_dim=128,
-            rope_theta=1e6, bits=4, k_group=32, v_group=32, n_prompts=1,
-            chunks_per_prompt=chunks, placement="prefix_hits", hit_chunks=hits,
-            seam_left=16, seam_right=16, probe_min_num=probe_min_pct, probe_min_den=100,
-            seed=seed * 100003 + i)
+        w = request_workload(i, chunks, hits, seed, n_layers, probe_min_pct)
         s = kw.structure(w)
-        draw = kw.layer_draws(w, s, 0)
-        di = pipeline.populate(w, s, draws_fn=lambda l: draw)
+        di = pipeline.populate(w, s, draws_fn=request_draws(w, s))
         pb = pipeline.buffers(di)
 
         def request():
-            if di.n_pool and di.n_probed:
-                pipeline.stitch_deviation(di, pb)
-            elif di.n_pool:
-                pipeline.stitch(di, pb)
-            pipeline.select(di, pb)
-            pipeline.patch(di, pb)
-            for li in range(di.n_layers):
-                pipeline.attn_layer(di, pb, li)
+            request_calls(di, pb)
 
         def timed(fn):
             a = torch.cuda.Event(enable_timing=True)

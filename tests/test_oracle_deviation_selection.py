@@ -154,3 +154,28 @@ def test_alg1_one_sided_window():
     for p in (128, 256, 384):
         expect[p - 16:p] = True
     assert np.array_equal(f, expect)
+
+
+def test_kth_margin_hand_worked():
+    """The margin at the top-k cut, worked by hand on values that are exact in
+    float32: prompt 0 ranks its five candidates 0.875 (row 1), 0.875 (row 2),
+    0.75, 0.5, 0.125 -- row 5 is live and its 0.8 must not enter; prompt 1
+    ranks 0.375, -0.0 (row 8) = +0.0 (row 9), then NaN; prompt 2 two +inf then
+    1; prompt 3 2, then two NaN."""
+    inf = float("inf")
+    d = np.array([0.5, 0.875, 0.875, 0.125, 0.75, 0.8,
+                  np.nan, 0.375, -0.0, 0.0,
+                  np.inf, np.inf, 1.0,
+                  np.nan, np.nan, 2.0], np.float32)
+    cu = np.array([0, 6, 10, 13, 16], np.int32)
+    cand = np.ones(16, bool)
+    cand[5] = False
+
+    def m(ks):
+        return selection.kth_margin(d, cand, cu, ks).tolist()
+
+    assert m([1, 1, 1, 1]) == [0.0, 0.375, 0.0, inf]      # equal values tie; number | NaN is wide
+    assert m([2, 2, 2, 2]) == [0.125, 0.0, inf, 0.0]      # -0 ties +0; inf | 1; NaN | NaN ties
+    assert m([3, 3, 0, 0]) == [0.25, inf, inf, inf]       # k = 0: no cut
+    assert m([4, 4, 3, 3]) == [0.375, inf, inf, inf]      # k = every candidate: no cut
+    assert m([5, 9, 9, 9]) == [inf, inf, inf, inf]        # prompt 0 has 5 candidates
