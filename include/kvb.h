@@ -90,11 +90,12 @@ typedef struct {
   int32_t pool_idx, src_pos, dst_row, dst_pos;
 } kvb_chunk;
 
-/* 5 for this header (version 2 added the optional fp16 shadow of V to
+/* 6 for this header (version 2 added the optional fp16 shadow of V to
  * kvb_stitch, kvb_sparse_attn and kvb_sparse_attn_workspace_bytes; version 3
  * added kvb_stitch_deviation and kvb_chunk_importance; version 4 added
  * kvb_probe_gate; version 5 added kvb_attn_plans_bytes, kvb_patch and
- * kvb_sparse_attn_layer). */
+ * kvb_sparse_attn_layer; version 6 added kvb_select_noalloc and
+ * kvb_select_noalloc_max_bytes). */
 int kvb_abi_version(void);
 
 /* Thread-local message of the last failing call on this thread. */
@@ -285,6 +286,25 @@ kvb_status kvb_select(int32_t n_sets, int64_t t_total, const int32_t* cu_seqlens
                       const float* delta, const uint8_t* row_flags,
                       const int32_t* k_per_seq, int32_t* rows, int32_t* cu_rows,
                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* kvb_select for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same selection, bit-identical outputs, with no workspace argument.  Its
+ * staging lives in a static device array of the library, one copy per device,
+ * held until the process ends; kvb_select_noalloc_max_bytes() returns its size
+ * (16 MiB).  The call allocates nothing.  Every call on a device shares that
+ * device's array (each call overwrites what it needs before reading it), so
+ * calls that overlap on one device race: order them on one stream.  Arguments
+ * as kvb_select without workspace / workspace_bytes.
+ * Errors: as kvb_select; KVB_EINVAL also when kvb_select_workspace_bytes(n_sets,
+ * t_total, n_seqs) exceeds kvb_select_noalloc_max_bytes(). */
+kvb_status kvb_select_noalloc(int32_t n_sets, int64_t t_total, const int32_t* cu_seqlens,
+                              int32_t n_seqs, const float* delta, const uint8_t* row_flags,
+                              const int32_t* k_per_seq, int32_t* rows, int32_t* cu_rows,
+                              void* stream);
+
+/* Bytes of the static scratch behind kvb_select_noalloc (pure function). */
+size_t kvb_select_noalloc_max_bytes(void);
 
 /* kvb_deviation then kvb_select on the same stream (Alg. 2 steps 2-3).
  * Arguments as in those two calls; delta is written as well. */

@@ -72,7 +72,7 @@ kvb_status check_pool(const kvb_pool_layout* p) {
 
 extern "C" {
 
-int kvb_abi_version(void) { return 5; }
+int kvb_abi_version(void) { return 6; }
 
 const char* kvb_last_error(void) { return g_err.c_str(); }
 
@@ -320,12 +320,14 @@ size_t kvb_select_workspace_bytes(int32_t n_sets, int64_t t_total, int32_t n_seq
 static kvb_status check_select(int32_t n_sets, int64_t t_total, const int32_t* cu_seqlens,
                                int32_t n_seqs, const float* delta, const uint8_t* row_flags,
                                const int32_t* k_per_seq, int32_t* rows, int32_t* cu_rows,
-                               void* workspace, size_t workspace_bytes) {
+                               void* workspace, size_t workspace_bytes,
+                               bool has_workspace = true) {
   REQUIRE(n_sets > 0 && n_sets <= 65535, "n_sets must be in [1, 65535]");
   REQUIRE(n_seqs > 0 && n_seqs <= 65535, "n_seqs must be in [1, 65535]");
   REQUIRE(t_total > 0 && t_total <= INT32_MAX, "t_total must be in (0, 2^31)");
   const void* ptrs[] = {cu_seqlens, delta, row_flags, k_per_seq, rows, cu_rows};
   for (const void* p : ptrs) REQUIRE(p != nullptr, "a required pointer is NULL");
+  if (!has_workspace) return KVB_OK;
   const size_t need = kvb::select_workspace_bytes(n_sets, t_total, n_seqs);
   REQUIRE(workspace_bytes >= need, "workspace %zu bytes, need %zu", workspace_bytes, need);
   if (need) REQUIRE(workspace != nullptr && aligned16(workspace), "workspace NULL or misaligned");
@@ -343,6 +345,29 @@ kvb_status kvb_select(int32_t n_sets, int64_t t_total, const int32_t* cu_seqlens
                                        k_per_seq, rows, cu_rows, workspace, (hipStream_t)stream),
                     "kvb_select");
 }
+
+kvb_status kvb_select_noalloc(int32_t n_sets, int64_t t_total, const int32_t* cu_seqlens,
+                              int32_t n_seqs, const float* delta, const uint8_t* row_flags,
+                              const int32_t* k_per_seq, int32_t* rows, int32_t* cu_rows,
+                              void* stream) {
+  REQUIRE(n_sets > 0 && n_sets <= 65535, "n_sets must be in [1, 65535]");
+  REQUIRE(n_seqs > 0 && n_seqs <= 65535, "n_seqs must be in [1, 65535]");
+  REQUIRE(t_total > 0 && t_total <= INT32_MAX, "t_total must be in (0, 2^31)");
+  const size_t need = kvb::select_workspace_bytes(n_sets, t_total, n_seqs);
+  REQUIRE(need <= kvb::kSelectScratchBytes,
+          "kvb_select_noalloc: %d sets x %lld rows need %zu bytes of scratch, more than its "
+          "%zu (use kvb_select with a workspace)",
+          n_sets, (long long)t_total, need, kvb::kSelectScratchBytes);
+  if (kvb_status s = check_select(n_sets, t_total, cu_seqlens, n_seqs, delta, row_flags,
+                                  k_per_seq, rows, cu_rows, nullptr, 0, /*has_workspace=*/false))
+    return s;
+  return hip_status(kvb::launch_select_noalloc(n_sets, t_total, cu_seqlens, n_seqs, delta,
+                                               row_flags, k_per_seq, rows, cu_rows,
+                                               (hipStream_t)stream),
+                    "kvb_select_noalloc");
+}
+
+size_t kvb_select_noalloc_max_bytes(void) { return kvb::kSelectScratchBytes; }
 
 kvb_status kvb_deviation_topk(int32_t n_layers, int32_t n_kv_heads, int32_t head_dim,
                               int64_t t_total, const int32_t* cu_seqlens, int32_t n_seqs,

@@ -52,6 +52,15 @@ hipError_t launch_select(int32_t n_sets, int64_t t_total, const int32_t* cu_seql
                          const int32_t* k_per_seq, int32_t* rows, int32_t* cu_rows,
                          void* workspace, hipStream_t s);
 
+// Allocation-free selection: the staging of kvb_select in a static device
+// array of kSelectScratchBytes bytes per device (no workspace argument).
+constexpr size_t kSelectScratchBytes = size_t(16) << 20;
+constexpr int kMaxDevices = 64;
+hipError_t launch_select_noalloc(int32_t n_sets, int64_t t_total, const int32_t* cu_seqlens,
+                                 int32_t n_seqs, const float* delta, const uint8_t* row_flags,
+                                 const int32_t* k_per_seq, int32_t* rows, int32_t* cu_rows,
+                                 hipStream_t s);
+
 struct AttnPlan {
   int rows_per_tile;   // selected rows per workgroup tile
   int tile_slots;      // tile slots per (layer, kv head)

@@ -21,6 +21,8 @@
 #include "kvb_device.h"
 #include "kvb_internal.h"
 
+#include <mutex>
+
 namespace kvb {
 namespace {
 
@@ -452,6 +454,46 @@ hipError_t launch_select(int32_t n_sets, int64_t t_total, const int32_t* cu_seql
     hipLaunchKernelGGL(pack_kernel, dim3(n_seqs, n_sets), dim3(256), 0, s, t_total, cu_seqlens,
                        n_seqs, staging, counts, rows, cu_rows);
   return hipGetLastError();
+}
+
+// Scratch of the allocation-free selection (kvb_select_noalloc): the staging
+// rows and per-prompt counts that kvb_select keeps in the caller's workspace.
+// Every device the library runs on holds one copy for the life of the process.
+// In host code `scratch` names a host-side stand-in, not device memory: host
+// code reaches the array only through the address select_scratch returns.
+static __device__ __align__(256) unsigned char scratch[kSelectScratchBytes];
+
+// Device address of this device's copy of `scratch`, looked up once per device
+// (with that device current) and kept.
+hipError_t select_scratch(void** ptr) {
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
+}
+
+hipError_t launch_select_noalloc(int32_t n_sets, int64_t t_total, const int32_t* cu_seqlens,
+                                 int32_t n_seqs, const float* delta, const uint8_t* row_flags,
+                                 const int32_t* k_per_seq, int32_t* rows, int32_t* cu_rows,
+                                 hipStream_t s) {
+  void* ws = nullptr;
+  if (n_seqs > 1) {
+    hipError_t e = select_scratch(&ws);
+    if (e != hipSuccess) return e;
+  }
+  return launch_select(n_sets, t_total, cu_seqlens, n_seqs, delta, row_flags, k_per_seq, rows,
+                       cu_rows, ws, s);
 }
 
 }  // namespace kvb

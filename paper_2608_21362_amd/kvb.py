@@ -58,6 +58,8 @@ _SIGS = {
     "kvb_deviation": (_i32, [_i32, _i32, _i32, _i64, _vp, _vp, _vp, _vp, _i32, _vp, _vp]),
     "kvb_select_workspace_bytes": (_sz, [_i32, _i64, _i32]),
     "kvb_select": (_i32, [_i32, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "kvb_select_noalloc": (_i32, [_i32, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "kvb_select_noalloc_max_bytes": (_sz, []),
     "kvb_deviation_topk": (_i32, [_i32, _i32, _i32, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _i32,
                                   _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "kvb_sparse_attn_workspace_bytes": (_sz, [_i32, _i32, _i32, _i32, _i64, _i32, _i32, _i32,
@@ -217,6 +219,17 @@ def kvb_select(n_sets, t_total, cu_seqlens, n_seqs, delta, row_flags, k_per_seq,
     _check(_lib.kvb_select(n_sets, t_total, _p(cu_seqlens), n_seqs, _p(delta), _p(row_flags),
                            _p(k_per_seq), _p(rows), _p(cu_rows), _p(workspace), workspace_bytes,
                            _stream(stream)))
+
+
+def kvb_select_noalloc(n_sets, t_total, cu_seqlens, n_seqs, delta, row_flags, k_per_seq, rows,
+                       cu_rows, stream=None):
+    _check(_lib.kvb_select_noalloc(n_sets, t_total, _p(cu_seqlens), n_seqs, _p(delta),
+                                   _p(row_flags), _p(k_per_seq), _p(rows), _p(cu_rows),
+                                   _stream(stream)))
+
+
+def kvb_select_noalloc_max_bytes():
+    return int(_lib.kvb_select_noalloc_max_bytes())
 
 
 def kvb_deviation_topk(n_layers, n_kv_heads, head_dim, t_total, cu_seqlens, n_seqs, k_cache,

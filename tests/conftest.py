@@ -15,5 +15,11 @@ def pytest_configure(config):
 
 def pytest_collection_modifyitems(config, items):
     # keep the full-size GPU cases after the small ones so a failure in a small
-    # case stops ``-x`` before the expensive ones start
-    items.sort(key=lambda it: 1 if "fullsize" in it.nodeid else 0)
+    # case stops ``-x`` before the expensive ones start; the allocation-free
+    # entry point's test runs last of all
+    def order(it):
+        if "test_zz_" in it.nodeid:
+            return 2
+        return 1 if "fullsize" in it.nodeid else 0
+
+    items.sort(key=order)

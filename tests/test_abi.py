@@ -33,7 +33,7 @@ def test_every_declared_symbol_is_exported():
     for n in names:
         assert hasattr(lib, n), n
     assert sorted(names) == sorted(kvb.EXPORTED)
-    assert kvb.kvb_abi_version() == 5
+    assert kvb.kvb_abi_version() == 6
 
 
 def test_ceiling_library_loads():
@@ -362,3 +362,22 @@ def test_valid_call_without_device_reports_hip_error():
     with pytest.raises(kvb.KvbError) as e:
         kvb.kvb_deviation(**_dev_args())
     assert e.value.status == kvb.KVB_EHIP and e.value.message
+
+
+def test_select_noalloc_rejects_sizes_beyond_its_scratch():
+    """The allocation-free selection refuses, before any HIP call, a batch
+    whose staging would not fit its static scratch, and checks its pointers
+    like kvb_select."""
+    lib = kvb.library()
+    cap = kvb.kvb_select_noalloc_max_bytes()
+    assert cap == 16 << 20
+    # 2 prompts: staging = sets x rows x 4 bytes (+ counts) > cap
+    t_big = cap // 4 + 1
+    st = lib.kvb_select_noalloc(1, t_big, FAKE, 2, FAKE, FAKE, FAKE, FAKE, FAKE, None)
+    assert st == kvb.KVB_EINVAL and b"scratch" in lib.kvb_last_error()
+    st = lib.kvb_select_noalloc(8, cap // 32, FAKE, 2, FAKE, FAKE, FAKE, FAKE, FAKE, None)
+    assert st == kvb.KVB_EINVAL
+    st = lib.kvb_select_noalloc(1, 1000, FAKE, 2, None, FAKE, FAKE, FAKE, FAKE, None)
+    assert st == kvb.KVB_EINVAL
+    st = lib.kvb_select_noalloc(0, 1000, FAKE, 2, FAKE, FAKE, FAKE, FAKE, FAKE, None)
+    assert st == kvb.KVB_EINVAL
