@@ -6,10 +6,11 @@ default one 8K-token prompt of the 36-layer Qwen2.5-3B-shaped workload
 random original offsets, 15 % per-layer recompute):
 
     kvb_stitch_deviation (all layers, one launch: dequantise + re-rotate the
-                          cached chunks, keep the fp16 shadow of V, and the
-                          per-layer K deviation of the stitched rows)
+                          cached chunks and the per-layer K deviation of the
+                          stitched rows)
     kvb_select           (all layers, one launch)
-    kvb_patch            (all layers, one launch; also the attention plans)
+    kvb_patch            (all layers: the patch and the attention plans in one
+                          launch, then the fp16 copy of every layer's V)
     kvb_sparse_attn_layer x 36 (one call per layer, as a model runs its layers)
 
 captured once in a HIP graph and replayed.  Inputs are resident in HBM before
@@ -21,8 +22,8 @@ on; "traffic" is the per-call HBM bytes from the committed rocprofv3 counter
 summary when it was taken on the current kernel sources.  ``rooflines`` adds
 the same figures for the bandwidth-bound calls (stitch, deviation, fused
 stitch + deviation) on the method's own bytes, timed with the Infinity Cache
-flushed; the fp16 shadow of V that the stitch also writes (the attention's
-P.V operand, not part of the method) is reported as an overhead next to them.
+flushed; the fp16 copy of V that the patch call builds for the attention
+(its P.V operand, not part of the method) is reported as an overhead.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--attn-all-layers] [--no-cpu-baseline]
@@ -56,17 +57,17 @@ def algorithmic(w, s, rows_per_set, cu_rows_per_set):
     statistics it reads and the bf16 K and V rows it writes.  Deviation (Alg. 2
     step 2): the stitched and fresh K rows it reads (bf16) and the deviation it
     writes.  Fused stitch + deviation: the stitch's bytes plus the fresh K rows
-    of the stitched chunks and their deviations.  The fp16 shadow of V, which
-    the stitch also writes for the attention's P.V operand, is not the
-    method's work: its bytes are returned separately.  Attention (Eq. 2):
-    4 d Hq flops per (selected query row, visible key): QK^T and PV."""
+    of the stitched chunks and their deviations.  The fp16 copy of V built for
+    the attention's P.V operand (the patched V cache read, the copy written)
+    is not the method's work: its bytes are returned separately.  Attention
+    (Eq. 2): 4 d Hq flops per (selected query row, visible key): QK^T and PV."""
     L, H, d, C, T, Hq = w.n_layers, w.n_kv_heads, w.head_dim, w.chunk_len, w.t_total, w.n_q_heads
     P = s.n_pool
     cb = d * w.bits // 8
     codes = 2 * P * L * H * C * cb
     stats = P * L * H * (C // w.k_group) * d * 8 + P * L * H * C * (d // w.v_group) * 8
     stitch_out = 2 * P * L * H * C * d * 2
-    shadow = P * L * H * C * d * 2
+    shadow = 2 * L * H * T * d * 2
     n_sets = rows_per_set.shape[0]
     fresh_k = P * L * H * C * d * 2
     b = {
@@ -401,13 +402,14 @@ def main():
     # timed call neither hits its inputs in the cache nor pays for another
     # kernel's write-back
     flush = torch.ones(args.flush_mb << 18, dtype=torch.float32, device="cuda")
-    flushed = {"stitch": [], "stitch_no_shadow": [], "deviation_topk": [], "deviation": [],
-               "stitch_deviation": []}
+    flushed = {"stitch": [], "deviation_topk": [], "deviation": [], "stitch_deviation": [],
+               "patch": [], "patch_no_copy": []}
     calls = {"stitch": lambda: pipeline.stitch(di, pb),
-             "stitch_no_shadow": lambda: pipeline.stitch(di, pb, shadow=False),
              "deviation_topk": lambda: pipeline.deviation_topk(di, pb),
              "deviation": lambda: pipeline.deviation(di, pb),
-             "stitch_deviation": lambda: pipeline.stitch_deviation(di, pb)}
+             "stitch_deviation": lambda: pipeline.stitch_deviation(di, pb),
+             "patch": lambda: pipeline.patch(di, pb),
+             "patch_no_copy": lambda: pipeline.patch(di, pb, f16_copy=False)}
     for _ in range(5):
         # flush, then the timed call right behind it on the same stream (no
         # host synchronisation in between, so the interval holds no idle
@@ -457,34 +459,28 @@ def main():
         committed_traffic(w.name, "traffic_bytes_per_launch" if patch_once
                           else "traffic_bytes_per_launch_with_patch"))
     def bw(name, key):
-        """Roofline figures of a bandwidth-bound call on the method's bytes (and,
-        next to them, on every byte it moves, the fp16 shadow of V included)."""
+        """Roofline figures of a bandwidth-bound call on the method's bytes."""
         by = nbytes[key]
         ms = fl_ms[name]
         gbs = by / (ms * 1e-3) / 1e9
-        total = nbytes[key] + (nbytes["shadow"] if key in ("stitch", "stitch_deviation") and
-                               name != "stitch_no_shadow" else 0)
-        r = {"bound": "hbm", "bytes": int(by), "us": ms * 1e3, "achieved": gbs,
-             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
-             "bytes_moved_incl_overhead": int(total),
-             "GBps_incl_overhead": total / (ms * 1e-3) / 1e9,
-             "frac_of_practical": practical_frac(total / (ms * 1e-3) / 1e9, total,
-                                                 nreads[key], ceil),
-             "timing": "median of 5 flushed calls (HIP events)"}
-        return r
+        return {"bound": "hbm", "bytes": int(by), "us": ms * 1e3, "achieved": gbs,
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
+                "frac_of_practical": practical_frac(gbs, by, nreads[key], ceil),
+                "timing": "median of 5 flushed calls (HIP events)"}
 
     rooflines = {
         "stitch": bw("stitch", "stitch"),
         "deviation": bw("deviation", "deviation"),
         "stitch_deviation": bw("stitch_deviation", "stitch_deviation"),
-        "stitch_without_shadow": bw("stitch_no_shadow", "stitch"),
     }
+    copy_us = (fl_ms["patch"] - fl_ms["patch_no_copy"]) * 1e3
     shadow_overhead = {
         "bytes": int(nbytes["shadow"]),
-        "what": "fp16 image of every stitched V row (the attention's P.V operand); written "
-                "by the stitch next to the method's bf16 cache",
-        "stitch_us_with": fl_ms["stitch"] * 1e3, "stitch_us_without": fl_ms["stitch_no_shadow"] * 1e3,
-        "us": (fl_ms["stitch"] - fl_ms["stitch_no_shadow"]) * 1e3,
+        "what": "fp16 copy of every layer's V (the attention's P.V operand), built by the "
+                "patch call from the patched bf16 V cache: V read, copy written",
+        "patch_us_with": fl_ms["patch"] * 1e3, "patch_us_without": fl_ms["patch_no_copy"] * 1e3,
+        "us": copy_us,
+        "GBps": nbytes["shadow"] / (copy_us * 1e-6) / 1e9 if copy_us > 0 else None,
     }
     tokens_per_step = w.t_total
     result = {

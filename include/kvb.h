@@ -15,8 +15,9 @@
  *   kvb_deviation_topk  kvb_deviation followed by kvb_select
  *   kvb_sparse_attn     patch the selected rows (Alg. 2 step 4), then causal
  *                       GQA attention of the selected query rows (Eq. 2)
- *   kvb_patch           Alg. 2 step 4 alone, every layer at once, and the
- *                       attention work plans of every layer
+ *   kvb_patch           Alg. 2 step 4 alone, every layer at once, with the
+ *                       attention's fp16 copy of V and work plans of every
+ *                       layer
  *   kvb_sparse_attn_layer  the repair forward's attention of one layer over
  *                       the patched cache (Eq. 2), with its prebuilt plan
  *
@@ -45,7 +46,7 @@
  *     (writing nothing) rather than read or write out of range.
  *   - Layouts (row-major, innermost last):
  *       cache K / V           bf16 [L][Hkv][T][d]      (T = t_total rows)
- *       fp16 shadow of V      fp16 [L][Hkv][T][d]      (optional; see kvb_stitch)
+ *       fp16 copy of V        fp16 [L][Hkv][T][d]      (see kvb_patch)
  *       queries / outputs     bf16 [L][T][Hq][d]
  *       chunk-pool codes      u8   [P][L][Hkv][C][d*b/8]
  *       key statistics        f32  [P][L][Hkv][C/Gk][d]    (scale, zero)
@@ -90,12 +91,15 @@ typedef struct {
   int32_t pool_idx, src_pos, dst_row, dst_pos;
 } kvb_chunk;
 
-/* 6 for this header (version 2 added the optional fp16 shadow of V to
+/* 7 for this header (version 2 added the optional fp16 shadow of V to
  * kvb_stitch, kvb_sparse_attn and kvb_sparse_attn_workspace_bytes; version 3
  * added kvb_stitch_deviation and kvb_chunk_importance; version 4 added
  * kvb_probe_gate; version 5 added kvb_attn_plans_bytes, kvb_patch and
  * kvb_sparse_attn_layer; version 6 added kvb_select_noalloc and
- * kvb_select_noalloc_max_bytes). */
+ * kvb_select_noalloc_max_bytes; version 7 moved the fp16 copy of V from the
+ * stitch to the patch: kvb_patch / kvb_sparse_attn build it from the patched
+ * cache, kvb_stitch and kvb_stitch_deviation no longer take it, and the
+ * building calls report values fp16 cannot hold in a status word). */
 int kvb_abi_version(void);
 
 /* Thread-local message of the last failing call on this thread. */
@@ -215,10 +219,6 @@ kvb_status kvb_chunk_importance(const kvb_pool_layout* pool, int32_t n_pool, int
  * outside the arrays is skipped.  n_pool bounds pool_idx; n_pool = 0 (nothing
  * cached: a cold prompt) is allowed with n_chunks = 0 and then the pool arrays
  * may be NULL (the call returns KVB_OK and writes nothing).
- * v_cache_f16 (optional, NULL for none; bf16 caches only): fp16 shadow of
- * v_cache, same layout; the stitched V rows are also stored there as the fp16
- * value of their bf16 result (exact while |v| <= 65504 and v is not below the
- * fp16 normal range).  kvb_sparse_attn reads V from such a shadow.
  * Errors: KVB_EINVAL, KVB_EUNSUPPORTED (bits not 4/8, d not 64/128, C != 128). */
 kvb_status kvb_stitch(const kvb_pool_layout* pool, int32_t n_pool,
                       const uint8_t* k_codes, const float* k_scale, const float* k_zero,
@@ -226,13 +226,13 @@ kvb_status kvb_stitch(const kvb_pool_layout* pool, int32_t n_pool,
                       const kvb_chunk* chunks, int32_t n_chunks,
                       const float* rope_cos, const float* rope_sin,
                       int64_t t_total, kvb_dtype out_dtype, void* k_cache, void* v_cache,
-                      uint16_t* v_cache_f16, void* stream);
+                      void* stream);
 
 /* kvb_stitch with a bf16 cache, fused with the per-layer deviation of the rows
  * it stitches (Alg. 2 steps 1-2 in one pass: the stitched keys are compared
  * with k_fresh while they are in registers instead of being read back).
- * Stitch outputs (k_cache, v_cache, optional v_cache_f16) are bit-identical
- * to kvb_stitch(..., KVB_BF16, ...).  For every row t of a chunk in the list
+ * Stitch outputs (k_cache, v_cache) are bit-identical to kvb_stitch(...,
+ * KVB_BF16, ...).  For every row t of a chunk in the list
  * and every layer l, delta[l][t] = 1 - (1/Hkv) sum_h cos(k_cache[l][h][t],
  * k_fresh[l][h][t]) with cos as in kvb_deviation (double sums over the bf16
  * values, the same zero-norm rule; the summation order differs, so values can
@@ -240,8 +240,8 @@ kvb_status kvb_stitch(const kvb_pool_layout* pool, int32_t n_pool,
  * 0 exactly).  K only, every layer its own set.  Rows outside the listed
  * chunks (live rows, whose cache already holds the fresh values) are not
  * written: kvb_select reads delta only at candidate rows, which are the
- * stitched rows.  k_cache, v_cache, v_cache_f16, k_fresh bf16/fp16
- * [L][Hkv][t_total][d]; delta f32 [L][t_total].
+ * stitched rows.  k_cache, v_cache, k_fresh bf16 [L][Hkv][t_total][d]; delta
+ * f32 [L][t_total].
  * Errors: as kvb_stitch (also the empty-pool rule); k_fresh and delta must be
  * non-NULL and aligned. */
 kvb_status kvb_stitch_deviation(const kvb_pool_layout* pool, int32_t n_pool,
@@ -249,8 +249,8 @@ kvb_status kvb_stitch_deviation(const kvb_pool_layout* pool, int32_t n_pool,
                                 const uint8_t* v_codes, const float* v_scale, const float* v_zero,
                                 const kvb_chunk* chunks, int32_t n_chunks,
                                 const float* rope_cos, const float* rope_sin, int64_t t_total,
-                                uint16_t* k_cache, uint16_t* v_cache, uint16_t* v_cache_f16,
-                                const uint16_t* k_fresh, float* delta, void* stream);
+                                uint16_t* k_cache, uint16_t* v_cache, const uint16_t* k_fresh,
+                                float* delta, void* stream);
 
 /* Per-token deviation (Alg. 2 step 2):
  *   delta[s][t] = 1 - (1/N) * sum cos(cache[l][h][t], fresh[l][h][t])
@@ -316,9 +316,21 @@ kvb_status kvb_deviation_topk(int32_t n_layers, int32_t n_kv_heads, int32_t head
                               int32_t* rows, int32_t* cu_rows, void* workspace,
                               size_t workspace_bytes, void* stream);
 
+/* The fp16 copy of V (the attention's P.V operand): fp16 [L][Hkv][T][d], each
+ * value the fp16 image of the bf16 V cache value at the same index (exact
+ * while |v| < 65536: a bf16 significand fits an fp16 one; bf16 values below
+ * 2^-14 become fp16 subnormals).  Built from the patched cache by kvb_patch
+ * (or inside kvb_sparse_attn).  Optional status word (v_status,
+ * DEVICE uint32, 4-byte aligned, NULL for none): the building call stores 1
+ * there when a V value fp16 cannot hold (|v| >= 65536, infinite or NaN) --
+ * the attention's P.V product would then see an infinity -- and never writes
+ * it otherwise, so the caller clears it before the call and reads it after
+ * (when it is 1 the outputs of those rows' prompts are not to be trusted:
+ * no fp16 variant of the product can hold such values). */
+
 /* Workspace bytes kvb_sparse_attn needs (pure function); v_f16_given is
- * non-zero when the call passes an fp16 shadow of V (the workspace then holds
- * no fp16 copy of V).  0 for invalid sizes. */
+ * non-zero when the call passes an fp16 copy of V (the workspace then holds none
+ * of its own).  0 for invalid sizes. */
 size_t kvb_sparse_attn_workspace_bytes(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads,
                                        int32_t head_dim, int64_t t_total, int32_t n_seqs,
                                        int32_t max_seq_len, int32_t max_rows,
@@ -328,23 +340,21 @@ size_t kvb_sparse_attn_workspace_bytes(int32_t n_layers, int32_t n_q_heads, int3
  * For each layer l and its row set S_l (rows[l] / cu_rows[l] when
  * rows_per_layer, else rows[0] / cu_rows[0] for every layer):
  *   1. k_cache[l][h][t] = k_fresh[l][h][t] and v_cache[l][h][t] = v_fresh[l][h][t]
- *      for every t in S_l and kv head h (and v_cache_f16[l][h][t] = fp16 of
- *      v_fresh[l][h][t] when the shadow is given);
- *   2. for every t in S_l and query head h, with g = floor(h * Hkv / Hq) and
+ *      for every t in S_l and kv head h;
+ *   2. the fp16 copy of the patched V cache of these layers, into
+ *      v_cache_f16 when given (n_layers x the layout above), else into the
+ *      workspace; v_status as described above;
+ *   3. for every t in S_l and query head h, with g = floor(h * Hkv / Hq) and
  *      b the prompt of t:
  *        out[l][t][h] = sum_{u = cu_seqlens[b]}^{t} softmax_u(scale * q[l][t][h] . K[l][g][u]) V[l][g][u]
  *      over the patched cache.  q is already rotated at the row's position.
  * QK^T runs as bf16 MFMA, the softmax in float (online, base-2 exponent), PV
- * as fp16 MFMA (probabilities and values converted to fp16; |V| must stay
- * within the fp16 range), accumulation in float.  V is read from v_cache_f16
- * when given (an fp16 shadow of v_cache that the caller keeps current for every
- * row not patched here -- kvb_stitch maintains it for the stitched rows);
- * otherwise the call converts v_cache into the workspace first.  Only rows of S_l are written
- * in out (bf16 or f32 per out_dtype, [L][t_total][Hq][d]).  max_rows bounds
- * |S_l| and max_seq_len bounds T_b (host values used to size the grid).
- * Deterministic: a tile's key ranges split between workgroups are combined in
- * key order.  Rows of S_l must be ascending within each prompt and belong to
- * it.
+ * as fp16 MFMA (probabilities and the copy of V in fp16), accumulation in
+ * float.  Only rows of S_l are written in out (bf16 or f32 per out_dtype,
+ * [L][t_total][Hq][d]).  max_rows bounds |S_l| and max_seq_len bounds T_b (host
+ * values used to size the grid).  Deterministic: a tile's key ranges split
+ * between workgroups are combined in key order.  Rows of S_l must be ascending
+ * within each prompt and belong to it.
  * Errors: KVB_EINVAL (incl. workspace too small, Hq % Hkv != 0),
  * KVB_EUNSUPPORTED (d not 64/128, Hq/Hkv not dividing 32). */
 kvb_status kvb_sparse_attn(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads,
@@ -353,8 +363,8 @@ kvb_status kvb_sparse_attn(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_hea
                            const int32_t* cu_rows, int32_t rows_per_layer, int32_t max_rows,
                            const uint16_t* q, const uint16_t* k_fresh, const uint16_t* v_fresh,
                            uint16_t* k_cache, uint16_t* v_cache, uint16_t* v_cache_f16,
-                           float softmax_scale, kvb_dtype out_dtype, void* out, void* workspace,
-                           size_t workspace_bytes, void* stream);
+                           uint32_t* v_status, float softmax_scale, kvb_dtype out_dtype, void* out,
+                           void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---- patch once, then attention layer by layer -------------------------
  * Alg. 2 takes the rows it patches (K~, V~) from the probe pass, which covers
@@ -362,8 +372,8 @@ kvb_status kvb_sparse_attn(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_hea
  * repair forward runs.  A caller that runs the repair forward layer by layer
  * can therefore patch every layer with one kvb_patch call right after the
  * selection, then make one kvb_sparse_attn_layer call per layer.  Results
- * (cache, fp16 shadow, out) are bit-identical to kvb_sparse_attn over the same
- * rows. */
+ * (cache, fp16 copy of V, out) are bit-identical to kvb_sparse_attn over the
+ * same rows. */
 
 /* Bytes of the plan buffer kvb_patch fills for n_layers layers (pure
  * function; 0 for invalid sizes).  The plans depend on the sizes given here and
@@ -374,21 +384,25 @@ size_t kvb_attn_plans_bytes(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_he
 
 /* Patch (Alg. 2 step 4) of every layer: for each layer l and t in S_l (rows[l]
  * / cu_rows[l] when rows_per_layer, else rows[0] / cu_rows[0]) and kv head h,
- * k_cache[l][h][t] = k_fresh[l][h][t], v_cache[l][h][t] = v_fresh[l][h][t] and,
- * when v_cache_f16 is given, v_cache_f16[l][h][t] = fp16 of v_fresh[l][h][t].
- * Layouts and sizes as kvb_sparse_attn.  When plans is not NULL the same launch
- * also writes the attention work plan of every layer into it (at least
- * kvb_attn_plans_bytes bytes, 16-byte aligned; the contents are opaque), for
- * the kvb_sparse_attn_layer calls that follow on the same rows.  Rows of S_l
- * must be ascending within each prompt and belong to it (as kvb_sparse_attn).
- * Errors: KVB_EINVAL (incl. plans smaller than kvb_attn_plans_bytes),
- * KVB_EUNSUPPORTED (as kvb_sparse_attn). */
+ * k_cache[l][h][t] = k_fresh[l][h][t] and v_cache[l][h][t] = v_fresh[l][h][t];
+ * then, when v_cache_f16 is given, the fp16 copy of every layer of the
+ * patched V cache (every row, whatever wrote it: the stitch, the caller's
+ * live rows, this patch), with the optional range status v_status (both as
+ * described above kvb_sparse_attn_workspace_bytes).  Layouts and sizes as
+ * kvb_sparse_attn.  When plans is not NULL the same launch also writes the
+ * attention work plan of every layer into it (at least kvb_attn_plans_bytes
+ * bytes, 16-byte aligned; the contents are opaque), for the
+ * kvb_sparse_attn_layer calls that follow on the same rows.  Rows of S_l must
+ * be ascending within each prompt and belong to it (as kvb_sparse_attn).
+ * Errors: KVB_EINVAL (incl. plans smaller than kvb_attn_plans_bytes, v_status
+ * without v_cache_f16), KVB_EUNSUPPORTED (as kvb_sparse_attn). */
 kvb_status kvb_patch(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
                      int64_t t_total, const int32_t* cu_seqlens, int32_t n_seqs,
                      int32_t max_seq_len, const int32_t* rows, const int32_t* cu_rows,
                      int32_t rows_per_layer, int32_t max_rows, const uint16_t* k_fresh,
                      const uint16_t* v_fresh, uint16_t* k_cache, uint16_t* v_cache,
-                     uint16_t* v_cache_f16, void* plans, size_t plans_bytes, void* stream);
+                     uint16_t* v_cache_f16, uint32_t* v_status, void* plans, size_t plans_bytes,
+                     void* stream);
 
 /* Attention (Eq. 2) of layer `layer` of n_layers for the rows of S_layer, over
  * the already patched cache: for every t in S_layer and query head h,
@@ -396,12 +410,12 @@ kvb_status kvb_patch(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, in
  *                      softmax_u(scale * q[layer][t][h] . K[layer][g][u]) V[layer][g][u]
  * with the arithmetic of kvb_sparse_attn.  Every pointer is the whole tensor
  * as kvb_sparse_attn takes it (the call offsets to the layer).  v_cache_f16 is
- * required (the fp16 shadow of V, current for every row, as kvb_stitch and
- * kvb_patch keep it); plans as filled by kvb_patch with the same sizes on this
- * device; workspace of at least kvb_sparse_attn_workspace_bytes(1, ...,
- * v_f16_given = 1) bytes (partial records; calls that share it must be ordered
- * on one stream).  Reads q, k_cache, v_cache_f16, rows, plans; writes out (rows
- * of S_layer only) and the workspace.
+ * required: the fp16 copy of the patched V cache (as kvb_patch builds
+ * them); plans as filled by kvb_patch with the same sizes on this device;
+ * workspace of at least kvb_sparse_attn_workspace_bytes(1, ..., v_f16_given =
+ * 1) bytes (partial records; calls that share it must be ordered on one
+ * stream).  Reads q, k_cache, v_cache_f16, rows, plans; writes out (rows of
+ * S_layer only) and the workspace.
  * Errors: KVB_EINVAL (incl. layer outside [0, n_layers), plans or workspace
  * too small, v_cache_f16 NULL), KVB_EUNSUPPORTED (as kvb_sparse_attn). */
 kvb_status kvb_sparse_attn_layer(int32_t layer, int32_t n_layers, int32_t n_q_heads,

@@ -72,7 +72,7 @@ kvb_status check_pool(const kvb_pool_layout* p) {
 
 extern "C" {
 
-int kvb_abi_version(void) { return 6; }
+int kvb_abi_version(void) { return 7; }
 
 const char* kvb_last_error(void) { return g_err.c_str(); }
 
@@ -228,7 +228,7 @@ kvb_status kvb_stitch(const kvb_pool_layout* pool, int32_t n_pool, const uint8_t
                       const float* v_scale, const float* v_zero, const kvb_chunk* chunks,
                       int32_t n_chunks, const float* rope_cos, const float* rope_sin,
                       int64_t t_total, kvb_dtype out_dtype, void* k_cache, void* v_cache,
-                      uint16_t* v_cache_f16, void* stream) {
+                      void* stream) {
   if (kvb_status s = check_pool(pool)) return s;
   REQUIRE(n_pool >= 0 && n_chunks >= 0, "n_pool and n_chunks must be non-negative");
   REQUIRE(n_pool > 0 || n_chunks == 0, "chunks listed with an empty pool");
@@ -239,18 +239,13 @@ kvb_status kvb_stitch(const kvb_pool_layout* pool, int32_t n_pool, const uint8_t
   // an empty pool (nothing cached) may come with NULL pool arrays
   for (size_t i = 0; i < (n_pool > 0 ? 8u : 2u); ++i)
     REQUIRE(ptrs[i] != nullptr && aligned16(ptrs[i]), "null or misaligned tensor");
-  if (v_cache_f16) {
-    REQUIRE(out_dtype == KVB_BF16, "an fp16 shadow of V goes with a bf16 cache");
-    REQUIRE(aligned16(v_cache_f16), "misaligned fp16 shadow of V");
-  }
   if (n_chunks == 0) return ok();
   REQUIRE(chunks != nullptr && rope_cos != nullptr && rope_sin != nullptr,
           "chunks and rotation tables are required");
   REQUIRE(aligned16(rope_cos) && aligned16(rope_sin), "rotation tables must be 16-byte aligned");
   return hip_status(kvb::launch_stitch(*pool, n_pool, k_codes, k_scale, k_zero, v_codes, v_scale,
                                        v_zero, chunks, n_chunks, rope_cos, rope_sin, t_total,
-                                       out_dtype, k_cache, v_cache, v_cache_f16,
-                                       (hipStream_t)stream),
+                                       out_dtype, k_cache, v_cache, (hipStream_t)stream),
                     "kvb_stitch");
 }
 
@@ -259,8 +254,8 @@ kvb_status kvb_stitch_deviation(const kvb_pool_layout* pool, int32_t n_pool,
                                 const uint8_t* v_codes, const float* v_scale, const float* v_zero,
                                 const kvb_chunk* chunks, int32_t n_chunks, const float* rope_cos,
                                 const float* rope_sin, int64_t t_total, uint16_t* k_cache,
-                                uint16_t* v_cache, uint16_t* v_cache_f16, const uint16_t* k_fresh,
-                                float* delta, void* stream) {
+                                uint16_t* v_cache, const uint16_t* k_fresh, float* delta,
+                                void* stream) {
   if (kvb_status s = check_pool(pool)) return s;
   REQUIRE(n_pool >= 0 && n_chunks >= 0, "n_pool and n_chunks must be non-negative");
   REQUIRE(n_pool > 0 || n_chunks == 0, "chunks listed with an empty pool");
@@ -271,15 +266,14 @@ kvb_status kvb_stitch_deviation(const kvb_pool_layout* pool, int32_t n_pool,
   // an empty pool (nothing cached) may come with NULL pool arrays
   for (size_t i = 0; i < (n_pool > 0 ? 10u : 4u); ++i)
     REQUIRE(ptrs[i] != nullptr && aligned16(ptrs[i]), "null or misaligned tensor");
-  if (v_cache_f16) REQUIRE(aligned16(v_cache_f16), "misaligned fp16 shadow of V");
   if (n_chunks == 0) return ok();
   REQUIRE(chunks != nullptr && rope_cos != nullptr && rope_sin != nullptr,
           "chunks and rotation tables are required");
   REQUIRE(aligned16(rope_cos) && aligned16(rope_sin), "rotation tables must be 16-byte aligned");
   return hip_status(kvb::launch_stitch_deviation(*pool, n_pool, k_codes, k_scale, k_zero, v_codes,
                                                  v_scale, v_zero, chunks, n_chunks, rope_cos,
-                                                 rope_sin, t_total, k_cache, v_cache, v_cache_f16,
-                                                 k_fresh, delta, (hipStream_t)stream),
+                                                 rope_sin, t_total, k_cache, v_cache, k_fresh,
+                                                 delta, (hipStream_t)stream),
                     "kvb_stitch_deviation");
 }
 
@@ -462,7 +456,8 @@ kvb_status kvb_patch(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, in
                      int32_t max_seq_len, const int32_t* rows, const int32_t* cu_rows,
                      int32_t rows_per_layer, int32_t max_rows, const uint16_t* k_fresh,
                      const uint16_t* v_fresh, uint16_t* k_cache, uint16_t* v_cache,
-                     uint16_t* v_cache_f16, void* plans, size_t plans_bytes, void* stream) {
+                     uint16_t* v_cache_f16, uint32_t* v_status, void* plans, size_t plans_bytes,
+                     void* stream) {
   if (kvb_status s = check_attn_sizes(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs,
                                       max_seq_len, max_rows))
     return s;
@@ -470,7 +465,9 @@ kvb_status kvb_patch(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, in
   for (const void* p : ptrs) REQUIRE(p != nullptr, "a required index pointer is NULL");
   const void* tens[] = {k_fresh, v_fresh, k_cache, v_cache};
   for (const void* p : tens) REQUIRE(p != nullptr && aligned16(p), "null or misaligned tensor");
-  if (v_cache_f16) REQUIRE(aligned16(v_cache_f16), "misaligned fp16 shadow of V");
+  if (v_cache_f16) REQUIRE(aligned16(v_cache_f16), "misaligned fp16 copy of V");
+  REQUIRE(v_status == nullptr || v_cache_f16 != nullptr, "v_status without an fp16 copy of V");
+  REQUIRE((reinterpret_cast<uintptr_t>(v_status) & 3u) == 0, "misaligned v_status");
   kvb::AttnPlan plan;
   if (kvb_status s = layer_plan(n_q_heads, n_kv_heads, head_dim, t_total, n_seqs, max_seq_len,
                                 max_rows, &plan))
@@ -480,11 +477,11 @@ kvb_status kvb_patch(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, in
     REQUIRE(plans_bytes >= need, "plans %zu bytes, need %zu", plans_bytes, need);
     REQUIRE(aligned16(plans), "misaligned plans");
   }
-  if (max_rows == 0) return ok();
+  if (max_rows == 0 && v_cache_f16 == nullptr) return ok();
   return hip_status(kvb::launch_patch_layers(plan, n_layers, n_kv_heads, head_dim, t_total,
                                              cu_seqlens, n_seqs, rows, cu_rows, rows_per_layer,
                                              max_rows, k_fresh, v_fresh, k_cache, v_cache,
-                                             v_cache_f16, plans, (hipStream_t)stream),
+                                             v_cache_f16, v_status, plans, (hipStream_t)stream),
                     "kvb_patch");
 }
 
@@ -532,8 +529,8 @@ kvb_status kvb_sparse_attn(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_hea
                            const int32_t* cu_rows, int32_t rows_per_layer, int32_t max_rows,
                            const uint16_t* q, const uint16_t* k_fresh, const uint16_t* v_fresh,
                            uint16_t* k_cache, uint16_t* v_cache, uint16_t* v_cache_f16,
-                           float softmax_scale, kvb_dtype out_dtype, void* out, void* workspace,
-                           size_t workspace_bytes, void* stream) {
+                           uint32_t* v_status, float softmax_scale, kvb_dtype out_dtype, void* out,
+                           void* workspace, size_t workspace_bytes, void* stream) {
   if (kvb_status s = check_attn_sizes(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs,
                                       max_seq_len, max_rows))
     return s;
@@ -543,7 +540,8 @@ kvb_status kvb_sparse_attn(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_hea
   for (const void* p : ptrs) REQUIRE(p != nullptr, "a required index pointer is NULL");
   const void* tens[] = {q, k_fresh, v_fresh, k_cache, v_cache, out};
   for (const void* p : tens) REQUIRE(p != nullptr && aligned16(p), "null or misaligned tensor");
-  if (v_cache_f16) REQUIRE(aligned16(v_cache_f16), "misaligned fp16 shadow of V");
+  if (v_cache_f16) REQUIRE(aligned16(v_cache_f16), "misaligned fp16 copy of V");
+  REQUIRE((reinterpret_cast<uintptr_t>(v_status) & 3u) == 0, "misaligned v_status");
   kvb::AttnPlan plan;
   if (!kvb::attn_plan(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs, max_seq_len,
                       max_rows, v_cache_f16 != nullptr, &plan))
@@ -551,12 +549,18 @@ kvb_status kvb_sparse_attn(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_hea
   REQUIRE(workspace_bytes >= plan.workspace, "workspace %zu bytes, need %zu", workspace_bytes,
           plan.workspace);
   if (plan.workspace) REQUIRE(workspace != nullptr && aligned16(workspace), "workspace NULL or misaligned");
-  if (max_rows == 0) return ok();
+  if (max_rows == 0) {
+    // nothing to patch or attend; a caller-kept fp16 copy of V still follows the cache
+    if (v_cache_f16 == nullptr) return ok();
+    return hip_status(kvb::launch_fp16_copy(n_layers, n_kv_heads, head_dim, t_total, v_cache,
+                                            v_cache_f16, v_status, (hipStream_t)stream),
+                      "kvb_sparse_attn");
+  }
   return hip_status(kvb::launch_sparse_attn(plan, n_layers, n_q_heads, n_kv_heads, head_dim,
                                             t_total, cu_seqlens, n_seqs, rows, cu_rows,
                                             rows_per_layer, max_rows, q, k_fresh, v_fresh, k_cache,
-                                            v_cache, v_cache_f16, softmax_scale, out_dtype, out,
-                                            workspace, (hipStream_t)stream),
+                                            v_cache, v_cache_f16, v_status, softmax_scale,
+                                            out_dtype, out, workspace, (hipStream_t)stream),
                     "kvb_sparse_attn");
 }
 

@@ -29,7 +29,7 @@ hipError_t launch_stitch(const kvb_pool_layout& p, int32_t n_pool, const uint8_t
                          const float* v_scale, const float* v_zero, const kvb_chunk* chunks,
                          int32_t n_chunks, const float* rope_cos, const float* rope_sin,
                          int64_t t_total, kvb_dtype out_dtype, void* k_cache, void* v_cache,
-                         uint16_t* v_cache_f16, hipStream_t s);
+                         hipStream_t s);
 
 // Stitch plus the per-layer K deviation of the stitched rows (bf16 cache).
 hipError_t launch_stitch_deviation(const kvb_pool_layout& p, int32_t n_pool,
@@ -38,8 +38,8 @@ hipError_t launch_stitch_deviation(const kvb_pool_layout& p, int32_t n_pool,
                                    const float* v_scale, const float* v_zero,
                                    const kvb_chunk* chunks, int32_t n_chunks,
                                    const float* rope_cos, const float* rope_sin, int64_t t_total,
-                                   void* k_cache, void* v_cache, uint16_t* v_cache_f16,
-                                   const uint16_t* k_fresh, float* delta, hipStream_t s);
+                                   void* k_cache, void* v_cache, const uint16_t* k_fresh,
+                                   float* delta, hipStream_t s);
 
 hipError_t launch_deviation(int n_layers, int n_kv_heads, int head_dim, int64_t t_total,
                             const uint16_t* k_cache, const uint16_t* k_fresh,
@@ -82,19 +82,25 @@ hipError_t launch_sparse_attn(const AttnPlan& plan, int n_layers, int n_q_heads,
                               int rows_per_layer, int max_rows, const uint16_t* q,
                               const uint16_t* k_fresh, const uint16_t* v_fresh,
                               uint16_t* k_cache, uint16_t* v_cache, uint16_t* v_cache_f16,
-                              float softmax_scale, kvb_dtype out_dtype, void* out, void* workspace,
-                              hipStream_t s);
+                              uint32_t* v_status, float softmax_scale, kvb_dtype out_dtype,
+                              void* out, void* workspace, hipStream_t s);
 
 // Bytes of one layer's plan in a buffer of per-layer plans (a multiple of 256).
 size_t layer_plan_stride(const AttnPlan& layer_plan);
 // Patch of n_layers layers; with plans != NULL also the per-layer plans
-// (layer_plan is the one-layer plan, the fp16 shadow of V given).
+// (layer_plan is the one-layer plan, the fp16 copy of V given), and with
+// v_cache_f16 != NULL the fp16 copy of the patched V cache.
 hipError_t launch_patch_layers(const AttnPlan& layer_plan, int n_layers, int n_kv_heads,
                                int head_dim, int64_t t_total, const int32_t* cu_seqlens,
                                int n_seqs, const int32_t* rows, const int32_t* cu_rows,
                                int rows_per_layer, int max_rows, const uint16_t* k_fresh,
                                const uint16_t* v_fresh, uint16_t* k_cache, uint16_t* v_cache,
-                               uint16_t* v_cache_f16, void* plans, hipStream_t s);
+                               uint16_t* v_cache_f16, uint32_t* v_status, void* plans,
+                               hipStream_t s);
+// fp16 copy of the V cache of n_layers layers; with status != NULL, 1 is
+// stored there when a value fp16 cannot hold is met.
+hipError_t launch_fp16_copy(int n_layers, int n_kv_heads, int head_dim, int64_t t_total,
+                            const uint16_t* v, uint16_t* v16, uint32_t* status, hipStream_t s);
 // Attention of layer `layer` over the patched cache with its prebuilt plan.
 hipError_t launch_sparse_attn_layer(const AttnPlan& layer_plan, int layer, int n_q_heads,
                                     int n_kv_heads, int head_dim, int64_t t_total,

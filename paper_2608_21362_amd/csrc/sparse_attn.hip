@@ -3,13 +3,13 @@
 // Per call, on one stream:
 //
 //   patch_kernel     cache[l][h][t] <- fresh[l][h][t] for every selected row t
-//                    (both tensors, every kv head), plus the fp16 image of the
-//                    new V rows when the caller keeps an fp16 shadow of V; its
-//                    first workgroup builds the work decomposition when the
-//                    launch uses balanced ranges (below)
-//   v16_kernel       only without a shadow: V of the call converted to fp16 in
-//                    the workspace (exact for |v| <= 65504: a bf16 significand
-//                    fits an fp16 one), so the P.V product takes fp16 operands
+//                    (both tensors, every kv head); its first workgroups build
+//                    the work decomposition when the launch uses balanced
+//                    ranges (below)
+//   v16_kernel       the fp16 copy of the patched V cache that the P.V product
+//                    takes as its operand (exact for |v| < 65536: a bf16
+//                    significand fits an fp16 one; values fp16 cannot hold are
+//                    reported in a status word)
 //   attn_kernel      the attention itself (below)
 //   combine_kernel   merges the partial records of tiles that were cut between
 //                    workgroups (balanced ranges only)
@@ -30,8 +30,8 @@
 //                                           other 16 sit in lane ^ 32.  The
 //                                           running maximum is refreshed only
 //                                           when a block raises it by more
-//                                           than 8 (log2 units), so partial
-//                                           probabilities stay below 2^8
+//                                           than 15 (log2 units), so partial
+//                                           probabilities stay below 2^15
 //   O^T (d x 32 queries) += V^T P^T        fp16 MFMA 32x32x16: V^T read from
 //                                           the row-major fp16 V block with the
 //                                           LDS transpose read, P^T converted
@@ -95,7 +95,12 @@ constexpr int kSegCost = 7;
 // gave the shortest launches, 7/5 and 13/10 about 1 % longer; a different
 // placement only costs balance, never correctness).
 constexpr int kFirstShareNum = 8, kFirstShareDen = 5;
-constexpr float kLazy = 8.0f;           // max growth (log2 units) tolerated before a rescale
+// Lazy rescaling: the running maximum (the reference of the probabilities)
+// moves only when a block's maximum exceeds it by more than kLazy log2 units,
+// so probabilities stay below 2^15 (fp16 holds up to 65504).  The reference
+// is never above the true maximum: a reference above it would push the
+// largest probabilities toward fp16's subnormal range.
+constexpr float kLazy = 15.0f;
 
 #define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
 
@@ -116,15 +121,29 @@ __device__ __forceinline__ void wait_lgkmcnt0() {
 __device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
 
 // ------------------------------------------------------------ V to fp16 ----
+// fp16 holds a bf16 value exactly unless its magnitude is 65536 or more (bf16
+// magnitude bits 0x4780 and up, infinities and NaN included).
+__device__ __forceinline__ bool f16_out_of_range(uint32_t w) {
+  return (w & 0x7FFFu) >= 0x4780u || ((w >> 16) & 0x7FFFu) >= 0x4780u;
+}
+
+// v16 <- fp16(v), n8 pieces of 8 values.  With status != NULL, a value fp16
+// cannot hold stores 1 there (plain stores of the same value by any thread
+// that found one; the caller clears the word).
 __global__ void __launch_bounds__(256)
-v16_kernel(int64_t n8, const uint16_t* __restrict__ v, uint16_t* __restrict__ v16) {
+v16_kernel(int64_t n8, const uint16_t* __restrict__ v, uint16_t* __restrict__ v16,
+           uint32_t* __restrict__ status) {
+  bool bad = false;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n8;
        i += (int64_t)gridDim.x * blockDim.x) {
     const uint4 a = reinterpret_cast<const uint4*>(v)[i];
+    bad |= f16_out_of_range(a.x) || f16_out_of_range(a.y) || f16_out_of_range(a.z) ||
+           f16_out_of_range(a.w);
     reinterpret_cast<uint4*>(v16)[i] =
         make_uint4(bf16x2_to_f16x2(a.x), bf16x2_to_f16x2(a.y),
                    bf16x2_to_f16x2(a.z), bf16x2_to_f16x2(a.w));
   }
+  if (status != nullptr && bad) *status = 1u;
 }
 
 // ------------------------------------------------------------ tile lookup --
@@ -350,7 +369,10 @@ __device__ __forceinline__ void softmax_block(f32x16 sacc, AttnState<D>& st, flo
   for (int r = 1; r < 16; ++r) bmax = fmaxf(bmax, sacc[r]);
   bmax = max_halves(bmax);
   const float m_new = fmaxf(st.m_raw, bmax);
-  const bool grow = (m_new - st.m_raw) * c_log2 > kLazy || st.m_raw == -INFINITY;
+  // a lane with no visible key yet (-inf before and after) does not force a
+  // rescale: its probabilities are 0 against any reference
+  const bool grow = (m_new - st.m_raw) * c_log2 > kLazy ||
+                    (st.m_raw == -INFINITY && m_new != -INFINITY);
   if (__builtin_expect(__builtin_amdgcn_ballot_w64(grow) != 0, 0)) {
     const float alpha = (st.m_raw == -INFINITY || m_new == -INFINITY)
                             ? (m_new == -INFINITY ? 1.0f : 0.0f)
@@ -723,8 +745,7 @@ __device__ __forceinline__ void build_plan(
 constexpr int kPatchRows = 4;  // row-list entries per patch wave
 
 // Patch: cache[l][h][t] <- fresh[l][h][t] for every selected row t (both
-// tensors, every kv head; one wave per kPatchRows rows), with the fp16 image of the new V
-// rows when the caller keeps an fp16 shadow of V.  With plan != NULL the first
+// tensors, every kv head; one wave per kPatchRows rows).  With plan != NULL the first
 // n_plans workgroups build work decompositions instead: one plan over all L
 // layers (n_plans = 1), or one plan per layer (n_plans = L, plan p at
 // plan + p * plan_stride, over layer p's row set alone).  n_tiles counts the
@@ -734,7 +755,7 @@ patch_kernel(int32_t L, int32_t Hkv, int32_t D, int64_t t_total, int32_t n_seqs,
              const int32_t* __restrict__ rows, const int32_t* __restrict__ cu_rows,
              int32_t rows_per_layer, int32_t max_rows, const uint16_t* __restrict__ kf,
              const uint16_t* __restrict__ vf, uint16_t* __restrict__ kc,
-             uint16_t* __restrict__ vc, uint16_t* __restrict__ vh,
+             uint16_t* __restrict__ vc,
              const int32_t* __restrict__ cu_seqlens, int32_t n_tiles, int32_t tile_slots,
              int32_t rows_per_tile, int32_t n_wg, int32_t n_first, int32_t n_wg_max,
              int32_t* __restrict__ plan, int32_t n_plans, int64_t plan_stride) {
@@ -793,15 +814,7 @@ patch_kernel(int32_t L, int32_t Hkv, int32_t D, int64_t t_total, int32_t n_seqs,
     for (int r = 0; r < kPatchRows; ++r) {
       if (!ok[r]) continue;
       const int64_t off = (base + t[r]) * D + c * 8;
-      if (tensor == 0) {
-        *reinterpret_cast<uint4*>(kc + off) = a[r];
-      } else {
-        *reinterpret_cast<uint4*>(vc + off) = a[r];
-        if (vh)
-          *reinterpret_cast<uint4*>(vh + off) =
-              make_uint4(bf16x2_to_f16x2(a[r].x), bf16x2_to_f16x2(a[r].y),
-                         bf16x2_to_f16x2(a[r].z), bf16x2_to_f16x2(a[r].w));
-      }
+      *reinterpret_cast<uint4*>((tensor == 0 ? kc : vc) + off) = a[r];
     }
   }
 }
@@ -1058,16 +1071,26 @@ void launch_patch(int n_layers, int n_kv_heads, int head_dim, int64_t t_total,
                   const int32_t* cu_seqlens, int n_seqs, const int32_t* rows,
                   const int32_t* cu_rows, int rows_per_layer, int max_rows,
                   const uint16_t* k_fresh, const uint16_t* v_fresh, uint16_t* k_cache,
-                  uint16_t* v_cache, uint16_t* v_f16, const AttnPlan& plan, int n_wg, int n_first,
+                  uint16_t* v_cache, const AttnPlan& plan, int n_wg, int n_first,
                   int32_t* plans, int n_plans, int64_t plan_stride, hipStream_t s) {
   const int64_t waves = (int64_t)n_layers * ((max_rows + kPatchRows - 1) / kPatchRows);
   const int64_t blocks = (waves * 64 + 255) / 256 + (plans ? n_plans : 0);
   if (blocks > 0)
     hipLaunchKernelGGL(patch_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n_layers, n_kv_heads,
                        head_dim, t_total, n_seqs, rows, cu_rows, rows_per_layer, max_rows, k_fresh,
-                       v_fresh, k_cache, v_cache, v_f16, cu_seqlens, plan.n_tiles, plan.tile_slots,
+                       v_fresh, k_cache, v_cache, cu_seqlens, plan.n_tiles, plan.tile_slots,
                        plan.rows_per_tile, n_wg, n_first, plan.n_wg_max, plans, n_plans,
                        plan_stride);
+}
+
+// fp16 copy of the V cache of n_layers layers (status as for v16_kernel).
+void launch_v16(int n_layers, int n_kv_heads, int head_dim, int64_t t_total, const uint16_t* v,
+                uint16_t* v16, uint32_t* status, hipStream_t s) {
+  const int64_t n8 = (int64_t)n_layers * n_kv_heads * t_total * head_dim / 8;
+  int64_t blocks = (n8 + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  if (blocks > 0)
+    hipLaunchKernelGGL(v16_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n8, v, v16, status);
 }
 
 // Attention (and, for balanced ranges, the merge of cut tiles) over an already
@@ -1110,8 +1133,8 @@ hipError_t launch_sparse_attn(const AttnPlan& plan, int n_layers, int n_q_heads,
                               int rows_per_layer, int max_rows, const uint16_t* q,
                               const uint16_t* k_fresh, const uint16_t* v_fresh,
                               uint16_t* k_cache, uint16_t* v_cache, uint16_t* v_cache_f16,
-                              float softmax_scale, kvb_dtype out_dtype, void* out, void* workspace,
-                              hipStream_t s) {
+                              uint32_t* v_status, float softmax_scale, kvb_dtype out_dtype,
+                              void* out, void* workspace, hipStream_t s) {
   char* wsb = reinterpret_cast<char*>(workspace);
   uint16_t* v16 = plan.v16_in_ws ? reinterpret_cast<uint16_t*>(wsb + plan.v16_offset) : v_cache_f16;
   int32_t* wplan = reinterpret_cast<int32_t*>(wsb + plan.plan_offset);
@@ -1120,18 +1143,18 @@ hipError_t launch_sparse_attn(const AttnPlan& plan, int n_layers, int n_q_heads,
   launch_shape(plan, &n_wg, &n_first);
   const bool balanced = is_balanced(plan, n_wg);
   launch_patch(n_layers, n_kv_heads, head_dim, t_total, cu_seqlens, n_seqs, rows, cu_rows,
-               rows_per_layer, max_rows, k_fresh, v_fresh, k_cache, v_cache,
-               plan.v16_in_ws ? nullptr : v_cache_f16, plan, n_wg, n_first,
+               rows_per_layer, max_rows, k_fresh, v_fresh, k_cache, v_cache, plan, n_wg, n_first,
                balanced ? wplan : nullptr, 1, 0, s);
-  if (plan.v16_in_ws) {
-    const int64_t n8 = (int64_t)n_layers * n_kv_heads * t_total * head_dim / 8;
-    int64_t blocks = (n8 + 255) / 256;
-    if (blocks > 8192) blocks = 8192;
-    hipLaunchKernelGGL(v16_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n8, v_cache, v16);
-  }
+  launch_v16(n_layers, n_kv_heads, head_dim, t_total, v_cache, v16, v_status, s);
   launch_attend(plan, n_wg, balanced, n_q_heads, n_kv_heads, head_dim, t_total, cu_seqlens, n_seqs,
                 rows, cu_rows, rows_per_layer, q, k_cache, v16, softmax_scale, out_dtype, out,
                 wplan, parts, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_fp16_copy(int n_layers, int n_kv_heads, int head_dim, int64_t t_total,
+                            const uint16_t* v, uint16_t* v16, uint32_t* status, hipStream_t s) {
+  launch_v16(n_layers, n_kv_heads, head_dim, t_total, v, v16, status, s);
   return hipGetLastError();
 }
 
@@ -1145,15 +1168,19 @@ hipError_t launch_patch_layers(const AttnPlan& layer_plan, int n_layers, int n_k
                                int n_seqs, const int32_t* rows, const int32_t* cu_rows,
                                int rows_per_layer, int max_rows, const uint16_t* k_fresh,
                                const uint16_t* v_fresh, uint16_t* k_cache, uint16_t* v_cache,
-                               uint16_t* v_cache_f16, void* plans, hipStream_t s) {
+                               uint16_t* v_cache_f16, uint32_t* v_status, void* plans,
+                               hipStream_t s) {
   int n_wg = 0, n_first = 0;
   launch_shape(layer_plan, &n_wg, &n_first);
   // plans are needed (and built) only for balanced ranges
   int32_t* p = (plans && is_balanced(layer_plan, n_wg)) ? reinterpret_cast<int32_t*>(plans) : nullptr;
-  launch_patch(n_layers, n_kv_heads, head_dim, t_total, cu_seqlens, n_seqs, rows, cu_rows,
-               rows_per_layer, max_rows, k_fresh, v_fresh, k_cache, v_cache, v_cache_f16,
-               layer_plan, n_wg, n_first, p, n_layers,
-               (int64_t)(layer_plan_stride(layer_plan) / sizeof(int32_t)), s);
+  if (max_rows > 0 || p != nullptr)
+    launch_patch(n_layers, n_kv_heads, head_dim, t_total, cu_seqlens, n_seqs, rows, cu_rows,
+                 rows_per_layer, max_rows, k_fresh, v_fresh, k_cache, v_cache, layer_plan, n_wg,
+                 n_first, p, n_layers,
+                 (int64_t)(layer_plan_stride(layer_plan) / sizeof(int32_t)), s);
+  if (v_cache_f16 != nullptr)
+    launch_v16(n_layers, n_kv_heads, head_dim, t_total, v_cache, v_cache_f16, v_status, s);
   return hipGetLastError();
 }
 

@@ -13,9 +13,6 @@
 // store a whole row and a wave's stores are contiguous.  Every value input of
 // the thread is loaded before the key work starts, so those loads overlap it.
 //
-// With a non-NULL fp16 shadow the value jobs also store the fp16 image of the
-// bfloat16 values (the operand the attention's P.V product reads).
-//
 // Arithmetic is double with contraction off: x = fma(code, scale, zero) is
 // exact in the product (8-bit code times 24-bit scale), so it equals the
 // product-then-sum form; the rotation is mul, mul, sub / add.  The double is
@@ -55,8 +52,8 @@ stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
               const float* __restrict__ v_scale, const float* __restrict__ v_zero,
               const kvb_chunk* __restrict__ chunks, const float* __restrict__ rope_cos,
               const float* __restrict__ rope_sin, int64_t t_total, void* __restrict__ k_out,
-              void* __restrict__ v_out, uint16_t* __restrict__ v16_out,
-              const uint16_t* __restrict__ k_fresh, float* __restrict__ delta) {
+              void* __restrict__ v_out, const uint16_t* __restrict__ k_fresh,
+              float* __restrict__ delta) {
   constexpr int H = D / 2;
   constexpr int CB = D * BITS / 8;       // code bytes per token row
   constexpr int TPT = H / 8;             // key threads per token quad
@@ -212,9 +209,6 @@ stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
         const uint4 A = make_uint4(pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]),
                                    pack_bf16x2(y[4], y[5]), pack_bf16x2(y[6], y[7]));
         *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(v_out) + o) = A;
-        if (v16_out)  // fp16 image of the bf16 values just written
-          *reinterpret_cast<uint4*>(v16_out + o) = make_uint4(bf16x2_to_f16x2(A.x), bf16x2_to_f16x2(A.y),
-                                                              bf16x2_to_f16x2(A.z), bf16x2_to_f16x2(A.w));
       } else {
         float* vo = reinterpret_cast<float*>(v_out) + o;
         *reinterpret_cast<float4*>(vo) = make_float4(y[0], y[1], y[2], y[3]);
@@ -253,14 +247,14 @@ hipError_t launch_stitch(const kvb_pool_layout& p, int32_t n_pool, const uint8_t
                          const float* v_scale, const float* v_zero, const kvb_chunk* chunks,
                          int32_t n_chunks, const float* rope_cos, const float* rope_sin,
                          int64_t t_total, kvb_dtype out_dtype, void* k_cache, void* v_cache,
-                         uint16_t* v_cache_f16, hipStream_t s) {
+                         hipStream_t s) {
   const dim3 grid(n_chunks, p.n_layers * p.n_kv_heads), block(256);
   const bool bf = out_dtype == KVB_BF16;
 #define KVB_STITCH(B, D, F)                                                                       \
   hipLaunchKernelGGL((stitch_kernel<B, D, F, false>), grid, block, 0, s, p.n_layers,             \
                      p.n_kv_heads, p.k_group, p.v_group, n_pool, k_codes, k_scale, k_zero,       \
                      v_codes, v_scale, v_zero, chunks, rope_cos, rope_sin, t_total, k_cache,     \
-                     v_cache, v_cache_f16, nullptr, nullptr)
+                     v_cache, nullptr, nullptr)
   if (p.bits == 8) {
     if (p.head_dim == 128) { if (bf) KVB_STITCH(8, 128, true); else KVB_STITCH(8, 128, false); }
     else { if (bf) KVB_STITCH(8, 64, true); else KVB_STITCH(8, 64, false); }
@@ -278,14 +272,14 @@ hipError_t launch_stitch_deviation(const kvb_pool_layout& p, int32_t n_pool,
                                    const float* v_scale, const float* v_zero,
                                    const kvb_chunk* chunks, int32_t n_chunks,
                                    const float* rope_cos, const float* rope_sin, int64_t t_total,
-                                   void* k_cache, void* v_cache, uint16_t* v_cache_f16,
-                                   const uint16_t* k_fresh, float* delta, hipStream_t s) {
+                                   void* k_cache, void* v_cache, const uint16_t* k_fresh,
+                                   float* delta, hipStream_t s) {
   const dim3 grid(n_chunks, p.n_layers), block(256);
 #define KVB_STITCH_DEV(B, D)                                                                      \
   hipLaunchKernelGGL((stitch_kernel<B, D, true, true>), grid, block, 0, s, p.n_layers,           \
                      p.n_kv_heads, p.k_group, p.v_group, n_pool, k_codes, k_scale, k_zero,       \
                      v_codes, v_scale, v_zero, chunks, rope_cos, rope_sin, t_total, k_cache,     \
-                     v_cache, v_cache_f16, k_fresh, delta)
+                     v_cache, k_fresh, delta)
   if (p.bits == 8) {
     if (p.head_dim == 128) KVB_STITCH_DEV(8, 128); else KVB_STITCH_DEV(8, 64);
   } else {

@@ -51,9 +51,9 @@ _SIGS = {
     "kvb_chunk_importance": (_i32, [ctypes.POINTER(kvb_pool_layout), _i32, _i32, _i32, _vp, _vp,
                                     _vp]),
     "kvb_stitch": (_i32, [ctypes.POINTER(kvb_pool_layout), _i32, _vp, _vp, _vp, _vp, _vp, _vp,
-                          _vp, _i32, _vp, _vp, _i64, _i32, _vp, _vp, _vp, _vp]),
+                          _vp, _i32, _vp, _vp, _i64, _i32, _vp, _vp, _vp]),
     "kvb_stitch_deviation": (_i32, [ctypes.POINTER(kvb_pool_layout), _i32, _vp, _vp, _vp, _vp,
-                                    _vp, _vp, _vp, _i32, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp,
+                                    _vp, _vp, _vp, _i32, _vp, _vp, _i64, _vp, _vp, _vp, _vp,
                                     _vp]),
     "kvb_deviation": (_i32, [_i32, _i32, _i32, _i64, _vp, _vp, _vp, _vp, _i32, _vp, _vp]),
     "kvb_select_workspace_bytes": (_sz, [_i32, _i64, _i32]),
@@ -65,11 +65,11 @@ _SIGS = {
     "kvb_sparse_attn_workspace_bytes": (_sz, [_i32, _i32, _i32, _i32, _i64, _i32, _i32, _i32,
                                               _i32]),
     "kvb_sparse_attn": (_i32, [_i32, _i32, _i32, _i32, _i64, _vp, _i32, _i32, _vp, _vp, _i32,
-                               _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _i32, _vp, _vp, _sz,
-                               _vp]),
+                               _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _i32, _vp, _vp,
+                               _sz, _vp]),
     "kvb_attn_plans_bytes": (_sz, [_i32, _i32, _i32, _i32, _i64, _i32, _i32, _i32]),
     "kvb_patch": (_i32, [_i32, _i32, _i32, _i32, _i64, _vp, _i32, _i32, _vp, _vp, _i32, _i32,
-                         _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+                         _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "kvb_sparse_attn_layer": (_i32, [_i32, _i32, _i32, _i32, _i32, _i64, _vp, _i32, _i32, _vp,
                                      _vp, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _f32, _i32, _vp,
                                      _vp, _sz, _vp]),
@@ -185,22 +185,20 @@ def kvb_chunk_importance(pool, n_pool, n_in, in_dtype, k_in, importance, stream=
 
 
 def kvb_stitch(pool, n_pool, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero, chunks,
-               n_chunks, rope_cos, rope_sin, t_total, out_dtype, k_cache, v_cache, v_cache_f16,
-               stream=None):
+               n_chunks, rope_cos, rope_sin, t_total, out_dtype, k_cache, v_cache, stream=None):
     _check(_lib.kvb_stitch(ctypes.byref(pool), n_pool, _p(k_codes), _p(k_scale), _p(k_zero),
                            _p(v_codes), _p(v_scale), _p(v_zero), _p(chunks), n_chunks,
                            _p(rope_cos), _p(rope_sin), t_total, out_dtype, _p(k_cache),
-                           _p(v_cache), _p(v_cache_f16), _stream(stream)))
+                           _p(v_cache), _stream(stream)))
 
 
 def kvb_stitch_deviation(pool, n_pool, k_codes, k_scale, k_zero, v_codes, v_scale, v_zero,
                          chunks, n_chunks, rope_cos, rope_sin, t_total, k_cache, v_cache,
-                         v_cache_f16, k_fresh, delta, stream=None):
+                         k_fresh, delta, stream=None):
     _check(_lib.kvb_stitch_deviation(ctypes.byref(pool), n_pool, _p(k_codes), _p(k_scale),
                                      _p(k_zero), _p(v_codes), _p(v_scale), _p(v_zero), _p(chunks),
                                      n_chunks, _p(rope_cos), _p(rope_sin), t_total, _p(k_cache),
-                                     _p(v_cache), _p(v_cache_f16), _p(k_fresh), _p(delta),
-                                     _stream(stream)))
+                                     _p(v_cache), _p(k_fresh), _p(delta), _stream(stream)))
 
 
 def kvb_deviation(n_layers, n_kv_heads, head_dim, t_total, k_cache, k_fresh, v_cache, v_fresh,
@@ -251,13 +249,13 @@ def kvb_sparse_attn_workspace_bytes(n_layers, n_q_heads, n_kv_heads, head_dim, t
 def kvb_sparse_attn(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, cu_seqlens, n_seqs,
                     max_seq_len, rows, cu_rows, rows_per_layer, max_rows, q, k_fresh, v_fresh,
                     k_cache, v_cache, v_cache_f16, softmax_scale, out_dtype, out, workspace,
-                    workspace_bytes, stream=None):
+                    workspace_bytes, stream=None, v_status=None):
     _check(_lib.kvb_sparse_attn(n_layers, n_q_heads, n_kv_heads, head_dim, t_total,
                                 _p(cu_seqlens), n_seqs, max_seq_len, _p(rows), _p(cu_rows),
                                 int(rows_per_layer), max_rows, _p(q), _p(k_fresh), _p(v_fresh),
-                                _p(k_cache), _p(v_cache), _p(v_cache_f16), float(softmax_scale),
-                                out_dtype, _p(out), _p(workspace), workspace_bytes,
-                                _stream(stream)))
+                                _p(k_cache), _p(v_cache), _p(v_cache_f16), _p(v_status),
+                                float(softmax_scale), out_dtype, _p(out), _p(workspace),
+                                workspace_bytes, _stream(stream)))
 
 
 def kvb_attn_plans_bytes(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_seqs, max_seq_len,
@@ -268,11 +266,12 @@ def kvb_attn_plans_bytes(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, n_s
 
 def kvb_patch(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, cu_seqlens, n_seqs,
               max_seq_len, rows, cu_rows, rows_per_layer, max_rows, k_fresh, v_fresh, k_cache,
-              v_cache, v_cache_f16, plans, plans_bytes, stream=None):
+              v_cache, v_cache_f16, plans, plans_bytes, stream=None, v_status=None):
     _check(_lib.kvb_patch(n_layers, n_q_heads, n_kv_heads, head_dim, t_total, _p(cu_seqlens),
                           n_seqs, max_seq_len, _p(rows), _p(cu_rows), int(rows_per_layer),
                           max_rows, _p(k_fresh), _p(v_fresh), _p(k_cache), _p(v_cache),
-                          _p(v_cache_f16), _p(plans), plans_bytes, _stream(stream)))
+                          _p(v_cache_f16), _p(v_status), _p(plans), plans_bytes,
+                          _stream(stream)))
 
 
 def kvb_sparse_attn_layer(layer, n_layers, n_q_heads, n_kv_heads, head_dim, t_total, cu_seqlens,

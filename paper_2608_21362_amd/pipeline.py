@@ -165,7 +165,7 @@ def populate(w: kw.Workload, s: kw.Structure, layers=None, with_q=True, draws_fn
 class PathBuffers:
     k_cache: torch.Tensor
     v_cache: torch.Tensor
-    v_cache_f16: torch.Tensor  # fp16 shadow of v_cache, kept by kvb_stitch and the patch
+    v_cache_f16: torch.Tensor  # fp16 copy of the patched v_cache (kvb_patch builds it)
     delta: torch.Tensor
     rows: torch.Tensor
     cu_rows: torch.Tensor
@@ -177,6 +177,7 @@ class PathBuffers:
     attn_ws_bytes_all: int = 0
     plans: torch.Tensor = None  # per-layer attention plans written by kvb_patch
     plans_bytes: int = 0
+    v_status: torch.Tensor = None  # uint32 word: set when a V value does not fit fp16
 
 
 def buffers(di: DeviceInputs, out_dtype=kvb.KVB_BF16, attn_all_layers=False) -> PathBuffers:
@@ -198,9 +199,8 @@ def buffers(di: DeviceInputs, out_dtype=kvb.KVB_BF16, attn_all_layers=False) -> 
         out.fill_(float("nan"))
     return PathBuffers(
         k_cache=di.cache_init_k.clone(), v_cache=di.cache_init_v.clone(),
-        # every prompt row is stitched (cached chunk) or selected (live rows are
-        # always selected), so each step rewrites the whole shadow
-        v_cache_f16=torch.zeros_like(di.cache_init_v),
+        v_cache_f16=torch.zeros((L, w.n_kv_heads, T, w.head_dim), dtype=torch.int16,
+                                device="cuda"),
         delta=torch.zeros((di.n_sets, T), dtype=torch.float32, device="cuda"),
         rows=torch.full((di.n_sets, T), -1, dtype=torch.int32, device="cuda"),
         cu_rows=torch.zeros((di.n_sets, B + 1), dtype=torch.int32, device="cuda"),
@@ -209,28 +209,26 @@ def buffers(di: DeviceInputs, out_dtype=kvb.KVB_BF16, attn_all_layers=False) -> 
         attn_ws=torch.empty(max(attn_bytes, 16), dtype=torch.uint8, device="cuda"),
         sel_ws_bytes=sel_bytes, attn_ws_bytes=per_layer_ws, attn_ws_bytes_all=all_ws,
         plans=torch.empty(max(plans_bytes, 16), dtype=torch.uint8, device="cuda"),
-        plans_bytes=plans_bytes)
+        plans_bytes=plans_bytes,
+        v_status=torch.zeros(4, dtype=torch.int32, device="cuda"))
 
 
 def stitch(di: DeviceInputs, pb: PathBuffers, out_dtype=kvb.KVB_BF16, k_out=None, v_out=None,
-           stream=None, shadow=True):
-    """Stitch into pb's bf16 cache (and its fp16 shadow of V unless ``shadow``
-    is False), or into ``k_out`` / ``v_out`` of ``out_dtype`` (no shadow)."""
-    own = k_out is None and v_out is None and out_dtype == kvb.KVB_BF16 and shadow
+           stream=None):
+    """Stitch into pb's bf16 cache, or into ``k_out`` / ``v_out`` of ``out_dtype``."""
     kvb.kvb_stitch(di.pool, di.n_pool, di.k_codes, di.k_scale, di.k_zero, di.v_codes, di.v_scale,
                    di.v_zero, di.chunks, di.n_pool, di.rope_cos, di.rope_sin, di.w.t_total,
                    out_dtype, pb.k_cache if k_out is None else k_out,
-                   pb.v_cache if v_out is None else v_out, pb.v_cache_f16 if own else None,
-                   stream)
+                   pb.v_cache if v_out is None else v_out, stream)
 
 
 def stitch_deviation(di: DeviceInputs, pb: PathBuffers, stream=None):
-    """Stitch (bf16 cache and fp16 shadow) fused with the per-layer deviation of
-    the stitched rows."""
+    """Stitch (bf16 cache) fused with the per-layer deviation of the stitched
+    rows."""
     kvb.kvb_stitch_deviation(di.pool, di.n_pool, di.k_codes, di.k_scale, di.k_zero, di.v_codes,
                              di.v_scale, di.v_zero, di.chunks, di.n_pool, di.rope_cos,
-                             di.rope_sin, di.w.t_total, pb.k_cache, pb.v_cache, pb.v_cache_f16,
-                             di.k_fresh, pb.delta, stream)
+                             di.rope_sin, di.w.t_total, pb.k_cache, pb.v_cache, di.k_fresh,
+                             pb.delta, stream)
 
 
 def select(di: DeviceInputs, pb: PathBuffers, stream=None):
@@ -265,19 +263,21 @@ def sparse_attn_layer(di: DeviceInputs, pb: PathBuffers, i: int, out_dtype=kvb.K
                         di.max_seq_len, pb.rows[si], pb.cu_rows[si], 0, di.max_rows, di.q[i],
                         di.k_fresh[i], di.v_fresh[i], pb.k_cache[i], pb.v_cache[i],
                         pb.v_cache_f16[i], 1.0 / float(np.sqrt(w.head_dim)), out_dtype, pb.out[i],
-                        pb.attn_ws,
-                        pb.attn_ws_bytes, stream)
+                        pb.attn_ws, pb.attn_ws_bytes, stream, v_status=pb.v_status)
 
 
-def patch(di: DeviceInputs, pb: PathBuffers, stream=None):
+def patch(di: DeviceInputs, pb: PathBuffers, stream=None, f16_copy=True):
     """Alg. 2 step 4 for every populated layer in one launch, which also builds
-    the per-layer attention plans that ``attn_layer`` reads."""
+    the per-layer attention plans that ``attn_layer`` reads, then (unless
+    ``f16_copy`` is False) the fp16 copy of the patched V cache, with the fp16
+    range status word."""
     w, T = di.w, di.w.t_total
     B = len(di.s.cu_seqlens) - 1
     kvb.kvb_patch(di.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, T, di.cu_seqlens, B,
                   di.max_seq_len, pb.rows, pb.cu_rows, int(w.per_layer), di.max_rows,
-                  di.k_fresh, di.v_fresh, pb.k_cache, pb.v_cache, pb.v_cache_f16, pb.plans,
-                  pb.plans_bytes, stream)
+                  di.k_fresh, di.v_fresh, pb.k_cache, pb.v_cache,
+                  pb.v_cache_f16 if f16_copy else None, pb.plans, pb.plans_bytes, stream,
+                  v_status=pb.v_status if f16_copy else None)
 
 
 def attn_layer(di: DeviceInputs, pb: PathBuffers, i: int, out_dtype=kvb.KVB_BF16, stream=None):
@@ -300,7 +300,7 @@ def sparse_attn_all(di: DeviceInputs, pb: PathBuffers, out_dtype=kvb.KVB_BF16, s
                         di.max_seq_len, pb.rows, pb.cu_rows, int(w.per_layer), di.max_rows, di.q,
                         di.k_fresh, di.v_fresh, pb.k_cache, pb.v_cache, pb.v_cache_f16,
                         1.0 / float(np.sqrt(w.head_dim)), out_dtype, pb.out, pb.attn_ws,
-                        pb.attn_ws_bytes_all, stream)
+                        pb.attn_ws_bytes_all, stream, v_status=pb.v_status)
 
 
 def run_path(di: DeviceInputs, pb: PathBuffers, attn_all_layers=False, out_dtype=kvb.KVB_BF16,

@@ -33,7 +33,7 @@ def test_every_declared_symbol_is_exported():
     for n in names:
         assert hasattr(lib, n), n
     assert sorted(names) == sorted(kvb.EXPORTED)
-    assert kvb.kvb_abi_version() == 6
+    assert kvb.kvb_abi_version() == 7
 
 
 def test_ceiling_library_loads():
@@ -89,7 +89,7 @@ def test_workspace_functions_are_pure():
     assert a == 0 and kvb.kvb_select_workspace_bytes(1, 32768, 16) > 32768 * 4
     x = kvb.kvb_sparse_attn_workspace_bytes(1, 16, 2, 128, 8192, 1, 8192, 1228, 0)
     assert x == kvb.kvb_sparse_attn_workspace_bytes(1, 16, 2, 128, 8192, 1, 8192, 1228, 0) and x > 0
-    # the fp16 copy of V (unless the caller keeps a shadow), the work
+    # the fp16 copy of V (unless the caller passes it), the work
     # decomposition and the partial records
     y = kvb.kvb_sparse_attn_workspace_bytes(36, 16, 2, 128, 8192, 1, 8192, 1228, 0)
     y16 = kvb.kvb_sparse_attn_workspace_bytes(36, 16, 2, 128, 8192, 1, 8192, 1228, 1)
@@ -107,8 +107,7 @@ def _pool(**kw_):
 def _stitch(**over):
     args = dict(pool=_pool(), n_pool=1, k_codes=FAKE, k_scale=FAKE, k_zero=FAKE, v_codes=FAKE,
                 v_scale=FAKE, v_zero=FAKE, chunks=FAKE, n_chunks=1, rope_cos=FAKE, rope_sin=FAKE,
-                t_total=128, out_dtype=kvb.KVB_BF16, k_cache=FAKE, v_cache=FAKE, v_cache_f16=None,
-                stream=0)
+                t_total=128, out_dtype=kvb.KVB_BF16, k_cache=FAKE, v_cache=FAKE, stream=0)
     args.update(over)
     kvb.kvb_stitch(**args)
 
@@ -125,8 +124,6 @@ def _stitch(**over):
     (dict(t_total=2**31), kvb.KVB_EINVAL),
     (dict(out_dtype=kvb.KVB_F64), kvb.KVB_EINVAL),
     (dict(rope_cos=None), kvb.KVB_EINVAL),
-    (dict(v_cache_f16=FAKE + 2), kvb.KVB_EINVAL),
-    (dict(v_cache_f16=FAKE, out_dtype=kvb.KVB_F32), kvb.KVB_EINVAL),  # shadow needs a bf16 cache
     (dict(n_pool=0), kvb.KVB_EINVAL),                  # chunks listed with an empty pool
     (dict(n_pool=-1, n_chunks=0), kvb.KVB_EINVAL),
     (dict(n_pool=0, n_chunks=0, k_cache=None), kvb.KVB_EINVAL),
@@ -149,8 +146,7 @@ def test_empty_pool_is_a_no_op():
 def _stitch_dev(**over):
     args = dict(pool=_pool(), n_pool=1, k_codes=FAKE, k_scale=FAKE, k_zero=FAKE, v_codes=FAKE,
                 v_scale=FAKE, v_zero=FAKE, chunks=FAKE, n_chunks=1, rope_cos=FAKE, rope_sin=FAKE,
-                t_total=128, k_cache=FAKE, v_cache=FAKE, v_cache_f16=None, k_fresh=FAKE,
-                delta=FAKE, stream=0)
+                t_total=128, k_cache=FAKE, v_cache=FAKE, k_fresh=FAKE, delta=FAKE, stream=0)
     args.update(over)
     kvb.kvb_stitch_deviation(**args)
 
@@ -162,7 +158,6 @@ def _stitch_dev(**over):
     (dict(delta=None), kvb.KVB_EINVAL),
     (dict(delta=FAKE + 4), kvb.KVB_EINVAL),
     (dict(k_cache=FAKE + 2), kvb.KVB_EINVAL),
-    (dict(v_cache_f16=FAKE + 2), kvb.KVB_EINVAL),
     (dict(t_total=0), kvb.KVB_EINVAL),
     (dict(rope_sin=None), kvb.KVB_EINVAL),
     (dict(n_pool=0), kvb.KVB_EINVAL),
@@ -236,6 +231,7 @@ def _attn(**over):
     (dict(softmax_scale=0.0), kvb.KVB_EINVAL),
     (dict(out_dtype=7), kvb.KVB_EINVAL),
     (dict(v_cache_f16=FAKE + 2), kvb.KVB_EINVAL),
+    (dict(v_status=FAKE + 2), kvb.KVB_EINVAL),          # status word not 4-byte aligned
 ])
 def test_sparse_attn_rejects(over, status):
     with pytest.raises(kvb.KvbError) as e:
@@ -295,6 +291,8 @@ def test_plans_bytes_is_pure_and_per_layer():
     (dict(rows=None), kvb.KVB_EINVAL),
     (dict(max_rows=5000), kvb.KVB_EINVAL),
     (dict(v_cache_f16=FAKE + 2), kvb.KVB_EINVAL),
+    (dict(v_status=FAKE + 1), kvb.KVB_EINVAL),
+    (dict(v_cache_f16=None, v_status=FAKE), kvb.KVB_EINVAL),  # a status needs the fp16 copy of V
 ])
 def test_patch_rejects(over, status):
     with pytest.raises(kvb.KvbError) as e:
@@ -323,9 +321,10 @@ def test_sparse_attn_layer_rejects(over, status):
 
 
 def test_patch_and_layer_without_rows_are_no_ops():
-    """max_rows = 0: nothing to patch or attend; both calls return before any
-    device work (so they succeed here, with no GPU)."""
-    _patch(max_rows=0)
+    """max_rows = 0: nothing to patch or attend; without an fp16 copy of V to
+    build both calls return before any device work (so they succeed here, with
+    no GPU)."""
+    _patch(max_rows=0, v_cache_f16=None)
     _attn_layer(max_rows=0)
 
 

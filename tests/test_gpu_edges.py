@@ -2,9 +2,10 @@
 through the C ABI, on generator-drawn inputs: out-of-range chunk descriptors;
 zero and negative-zero vectors, identical rows, values in the deviation,
 all-layer deviation; ragged batches with empty prompts, one-row prompts and
-prompts with no selected row, both head sizes, with and without the fp16
-shadow of V.  Stitch bit-exact; deviation within one float32 ulp of the
-oracle; selection bit-exact; patch bit-exact; attention within
+prompts with no selected row, both head sizes, the fp16 copy of V in a
+caller buffer or in the workspace; the fp16 range flag.  Stitch bit-exact;
+deviation within one float32 ulp of the oracle; selection bit-exact; patch
+and the fp16 copy of V bit-exact; attention within
 |o - o_ref| <= 2e-2 + 1e-2 |o_ref|; rows that are not selected never written."""
 import sys
 
@@ -18,6 +19,11 @@ from oracle import numerics, selection as osel
 
 pytestmark = pytest.mark.gpu
 ATOL, RTOL = 2e-2, 1e-2
+
+
+def _f16_of_bf16(bits):
+    """fp16 bit patterns of bf16 values (numpy's float32 -> float16, RNE)."""
+    return numerics.bf16_bits_to_f32(bits).astype(np.float16).view(np.uint16)
 LENS = [0, 37, 0, 129, 1, 640, 0, 255, 3]
 
 
@@ -98,9 +104,13 @@ def test_attention_ragged_with_empty_prompts(hq, hkv, d, shadow, split):
     cu_rows = np.searchsorted(rows, cu).astype(np.int32)
     max_seq = int(np.max(np.diff(cu)))
     dk, dv = torch.from_numpy(kc.view(np.int16)).cuda(), torch.from_numpy(vc.view(np.int16)).cuda()
+    # shadow: the call builds the fp16 copy of V into a caller buffer (filled
+    # with NaN patterns first; else into its workspace); a range status word
+    # rides along
     v16 = None
     if shadow:
-        v16 = torch.from_numpy(numerics.bf16_bits_to_f32(vc).astype(np.float16).view(np.int16)).cuda()
+        v16 = torch.full((hkv, T, d), 0x7E00, dtype=torch.int16, device="cuda")
+    status = torch.zeros(4, dtype=torch.int32, device="cuda")
     out = torch.full((T, hq, d), -1, dtype=torch.int16, device="cuda")
     wsb = kvb.kvb_sparse_attn_workspace_bytes(1, hq, hkv, d, T, B, max_seq, len(rows), int(shadow))
     ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
@@ -111,20 +121,21 @@ def test_attention_ragged_with_empty_prompts(hq, hkv, d, shadow, split):
         pbytes = kvb.kvb_attn_plans_bytes(1, hq, hkv, d, T, B, max_seq, len(rows))
         plans = torch.empty(max(pbytes, 16), dtype=torch.uint8, device="cuda")
         kvb.kvb_patch(1, hq, hkv, d, T, dcu, B, max_seq, drows, dcur, 0, len(rows), dkf, dvf, dk,
-                      dv, v16, plans, pbytes)
+                      dv, v16, plans, pbytes, v_status=status if shadow else None)
         kvb.kvb_sparse_attn_layer(0, 1, hq, hkv, d, T, dcu, B, max_seq, drows, dcur, 0, len(rows),
                                   dq, dk, v16, plans, pbytes, 1.0 / np.sqrt(d), kvb.KVB_BF16, out,
                                   ws, wsb)
     else:
         kvb.kvb_sparse_attn(1, hq, hkv, d, T, dcu, B, max_seq, drows, dcur, 0, len(rows), dq, dkf,
-                            dvf, dk, dv, v16, 1.0 / np.sqrt(d), kvb.KVB_BF16, out, ws, wsb)
+                            dvf, dk, dv, v16, 1.0 / np.sqrt(d), kvb.KVB_BF16, out, ws, wsb,
+                            v_status=status)
     torch.cuda.synchronize()
     pk, pv = oatt.patch(kc, kf, rows), oatt.patch(vc, vf, rows)
     assert np.array_equal(dk.cpu().numpy().view(np.uint16), pk)
     assert np.array_equal(dv.cpu().numpy().view(np.uint16), pv)
     if shadow:
-        assert np.array_equal(v16.cpu().numpy().view(np.uint16),
-                              numerics.bf16_bits_to_f32(pv).astype(np.float16).view(np.uint16))
+        assert np.array_equal(v16.cpu().numpy().view(np.uint16), _f16_of_bf16(pv))
+    assert int(status[0].item()) == 0
     ref = oatt.attend_rows(q, pk, pv, rows, cu)
     o = out.cpu().numpy().view(np.uint16)
     got = numerics.bf16_bits_to_f32(o[rows]).astype(np.float64)
@@ -208,3 +219,42 @@ def test_stitch_skips_out_of_range_descriptors():
     ostitch.stitch_into(ck, cv, ref.pool, ref.chunks, ref.cos, ref.sin, "bf16")
     assert np.array_equal(pb.k_cache.cpu().numpy().view(np.uint16), ck)
     assert np.array_equal(pb.v_cache.cpu().numpy().view(np.uint16), cv)
+
+
+@pytest.mark.parametrize("where", ["patched", "stitched"])
+def test_fp16_range_flag(where):
+    """A V value fp16 cannot hold (|v| = 1e5: 99840 in bf16) in a patched row
+    or in a row the patch leaves alone sets the status word of kvb_patch; the
+    same cache without it leaves the word at 0."""
+    _need_gpu()
+    from paper_2608_21362_amd import kvb
+
+    rng = np.random.default_rng(5)
+    hq, hkv, d, T = 16, 2, 128, 300
+    cu = np.array([0, T], np.int32)
+    kc, vc = _bf16(rng, (hkv, T, d)), _bf16(rng, (hkv, T, d))
+    kf, vf = _bf16(rng, (hkv, T, d)), _bf16(rng, (hkv, T, d))
+    rows = np.arange(0, T, 3, dtype=np.int32)
+    cu_rows = np.array([0, len(rows)], np.int32)
+    for planted in (False, True):
+        vc2, vf2 = vc.copy(), vf.copy()
+        if planted:
+            big = numerics.f32_to_bf16_bits(np.array([1e5], np.float32))[0]
+            if where == "patched":
+                vf2[1, rows[7], 5] = big
+            else:
+                vc2[0, 4, 17] = big  # row 4 is not selected
+        dk, dv = (torch.from_numpy(x.view(np.int16)).cuda() for x in (kc, vc2))
+        dkf, dvf = (torch.from_numpy(x.view(np.int16)).cuda() for x in (kf, vf2))
+        v16 = torch.zeros((hkv, T, d), dtype=torch.int16, device="cuda")
+        status = torch.zeros(4, dtype=torch.int32, device="cuda")
+        pbytes = kvb.kvb_attn_plans_bytes(1, hq, hkv, d, T, 1, T, len(rows))
+        plans = torch.empty(max(pbytes, 16), dtype=torch.uint8, device="cuda")
+        dcu, drows, dcur = (torch.from_numpy(x).cuda() for x in (cu, rows, cu_rows))
+        kvb.kvb_patch(1, hq, hkv, d, T, dcu, 1, T, drows, dcur, 0, len(rows), dkf, dvf, dk, dv,
+                      v16, plans, pbytes, v_status=status)
+        torch.cuda.synchronize()
+        flag = int(status[0].item())
+        _say(f"[fp16-range] {where} planted={planted}: flag {flag}")
+        assert flag == (1 if planted else 0)
+        assert np.all(status.cpu().numpy()[1:] == 0)

@@ -2,15 +2,15 @@
 batched 16 x 2048 workload and the 36-layer 32K workload (4 sinks, seams on
 both sides), in the launch configuration bench.py times (one fused stitch +
 deviation and one selection for all layers, one patch of every layer, then one
-attention call per layer with the fp16 shadow of V); the 8K workload also in
+attention call per layer over the fp16 copy of V); the 8K workload also in
 bench.py's --unfused configuration (one stitch, then one deviation +
 selection).
 
 Checks per layer, against the oracle built from the same seeded draws:
-stitch bit-exact (K, V and the fp16 shadow of the stitched V), deviation
-within 1 fp32 ulp, selection by the margin / band rule of
-``selection_check``, patch bit-exact on the GPU's own row set, the shadow
-equal to the fp16 image of the final V cache, and attention within
+stitch bit-exact (K and V), deviation within 1 fp32 ulp, selection by the
+margin / band rule of ``selection_check``, patch bit-exact on the GPU's own
+row set, the fp16 copy of V equal to the fp16 image of the patched V cache
+(no range flag), and attention within
 |o - o_ref| <= 2e-2 + 1e-2 |o_ref| on a sample of selected rows (every
 selected row on the first and last layer of the 8K workload; on the 32K
 workload the attention of layers 0, 17 and 35 only, whose queries are the
@@ -80,11 +80,11 @@ def test_fullsize(name, n_sample, full, fused, attn_layers):
     if fused:
         # deviations of live rows stay at the buffer's zeros, which is their value
         pipeline.stitch_deviation(dev, pb)
-        st_k, st_v, st_v16 = pb.k_cache.clone(), pb.v_cache.clone(), pb.v_cache_f16.clone()
+        st_k, st_v = pb.k_cache.clone(), pb.v_cache.clone()
         pipeline.select(dev, pb)
     else:
         pipeline.stitch(dev, pb)
-        st_k, st_v, st_v16 = pb.k_cache.clone(), pb.v_cache.clone(), pb.v_cache_f16.clone()
+        st_k, st_v = pb.k_cache.clone(), pb.v_cache.clone()
         pipeline.deviation_topk(dev, pb)
     # the launch configuration bench.py times: one patch of every layer, then
     # one attention call per layer
@@ -93,6 +93,7 @@ def test_fullsize(name, n_sample, full, fused, attn_layers):
         pipeline.attn_layer(dev, pb, i)
     torch.cuda.synchronize()
     _say(f"[fullsize] {name}: GPU path done")
+    assert int(pb.v_status[0].item()) == 0, "fp16 range flag set on in-range values"
     rows_all = pb.rows.cpu().numpy()
     cu_all = pb.cu_rows.cpu().numpy()
     delta = pb.delta.cpu().numpy()
@@ -106,11 +107,10 @@ def test_fullsize(name, n_sample, full, fused, attn_layers):
         ref = opop.populate(w, s, layers=[l], with_q=attend)
         ck, cv = ref.cache_k.copy(), ref.cache_v.copy()
         ostitch.stitch_into(ck, cv, ref.pool, ref.chunks, ref.cos, ref.sin, "bf16")
-        # stitch (before the patch), with the fp16 shadow of the stitched V rows
-        gk0, gv0, gh0 = _np16(st_k[i]), _np16(st_v[i]), _np16(st_v16[i])
+        # stitch (before the patch)
+        gk0, gv0 = _np16(st_k[i]), _np16(st_v[i])
         assert np.array_equal(gk0, ck[0]), f"layer {l}: stitched K"
         assert np.array_equal(gv0, cv[0]), f"layer {l}: stitched V"
-        assert np.array_equal(gh0[:, hit], _f16_of_bf16(cv[0][:, hit])), f"layer {l}: fp16 shadow"
         # deviation
         rd32 = odev.deviation(ck, ref.k_fresh, per_layer=True)[0].astype(np.float32)
         gd = delta[i]
@@ -128,12 +128,13 @@ def test_fullsize(name, n_sample, full, fused, attn_layers):
                                  where=f"{name} layer {l}")
         if n_band:
             _say(f"[fullsize] {name} layer {l}: {n_band} prompts differ inside the band")
-        # patch on the GPU's rows; the shadow is the fp16 image of the final V
+        # patch on the GPU's rows; the fp16 copy is the image of the patched V
         pk = oatt.patch(ck[0], ref.k_fresh[0], g_rows)
         pv = oatt.patch(cv[0], ref.v_fresh[0], g_rows)
-        gk, gv, gh = _np16(pb.k_cache[i]), _np16(pb.v_cache[i]), _np16(pb.v_cache_f16[i])
+        gk, gv = _np16(pb.k_cache[i]), _np16(pb.v_cache[i])
         assert np.array_equal(gk, pk) and np.array_equal(gv, pv), f"layer {l}: patch"
-        assert np.array_equal(gh, _f16_of_bf16(gv)), f"layer {l}: fp16 shadow after the patch"
+        gh = _np16(pb.v_cache_f16[i])
+        assert np.array_equal(gh, _f16_of_bf16(pv)), f"layer {l}: fp16 copy of V"
         # attention
         if not attend:
             _say(f"[fullsize] {name} layer {l}: stitch, deviation, selection, patch ok")
