@@ -123,20 +123,32 @@ stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
           cs[k] = cc.x; cs[k + 1] = cc.y; cs[k + 2] = cc.z; cs[k + 3] = cc.w;
           sn[k] = ss.x; sn[k + 1] = ss.y; sn[k + 2] = ss.z; sn[k + 3] = ss.w;
         }
+        // the codes of the four tokens (and, fused, their fresh key pieces)
+        // are all requested before any is used: one memory round trip per job
+        uint32_t cwl[4][2], cwh[4][2];
+        uint4 fra[4], frb[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int u = u0 + i;
-          const uint8_t* row = k_codes + (slab * kC + u) * CB;
-          uint32_t wl[2], wh[2];
+          const uint8_t* row = k_codes + (slab * kC + u0 + i) * CB;
           if constexpr (BITS == 8) {
             const uint2 a = *reinterpret_cast<const uint2*>(row + j0);
             const uint2 b = *reinterpret_cast<const uint2*>(row + H + j0);
-            wl[0] = a.x; wl[1] = a.y; wh[0] = b.x; wh[1] = b.y;
+            cwl[i][0] = a.x; cwl[i][1] = a.y; cwh[i][0] = b.x; cwh[i][1] = b.y;
           } else {
-            wl[0] = *reinterpret_cast<const uint32_t*>(row + j0 / 2);
-            wh[0] = *reinterpret_cast<const uint32_t*>(row + (H + j0) / 2);
-            wl[1] = wh[1] = 0;
+            cwl[i][0] = *reinterpret_cast<const uint32_t*>(row + j0 / 2);
+            cwh[i][0] = *reinterpret_cast<const uint32_t*>(row + (H + j0) / 2);
+            cwl[i][1] = cwh[i][1] = 0;
           }
+          if constexpr (DEV) {
+            const uint16_t* fr = k_fresh + (out_row0 + u0 + i) * D;
+            fra[i] = *reinterpret_cast<const uint4*>(fr + j0);
+            frb[i] = *reinterpret_cast<const uint4*>(fr + H + j0);
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int u = u0 + i;
+          const uint32_t wl[2] = {cwl[i][0], cwl[i][1]}, wh[2] = {cwh[i][0], cwh[i][1]};
           float ylo[8], yhi[8];
 #pragma unroll
           for (int k = 0; k < 8; ++k) {
@@ -160,9 +172,7 @@ stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
             *reinterpret_cast<uint4*>(ko + j0) = A;
             *reinterpret_cast<uint4*>(ko + H + j0) = B;
             if constexpr (DEV) {
-              const uint16_t* fr = k_fresh + o;
-              const uint4 FA = *reinterpret_cast<const uint4*>(fr + j0);
-              const uint4 FB = *reinterpret_cast<const uint4*>(fr + H + j0);
+              const uint4 FA = fra[i], FB = frb[i];
               const uint32_t cw[8] = {A.x, A.y, A.z, A.w, B.x, B.y, B.z, B.w};
               const uint32_t fw[8] = {FA.x, FA.y, FA.z, FA.w, FB.x, FB.y, FB.z, FB.w};
               double dot = 0.0, na = 0.0, nb = 0.0;
