@@ -22,8 +22,10 @@ ATOL, RTOL = 2e-2, 1e-2
 
 
 def _f16_of_bf16(bits):
-    """fp16 bit patterns of bf16 values (numpy's float32 -> float16, RNE)."""
-    return numerics.bf16_bits_to_f32(bits).astype(np.float16).view(np.uint16)
+    """fp16 bit patterns of bf16 values (numpy's float32 -> float16, RNE;
+    magnitudes past fp16's range become infinities, as on the device)."""
+    with np.errstate(over="ignore"):
+        return numerics.bf16_bits_to_f32(bits).astype(np.float16).view(np.uint16)
 LENS = [0, 37, 0, 129, 1, 640, 0, 255, 3]
 
 
@@ -258,3 +260,46 @@ def test_fp16_range_flag(where):
         _say(f"[fp16-range] {where} planted={planted}: flag {flag}")
         assert flag == (1 if planted else 0)
         assert np.all(status.cpu().numpy()[1:] == 0)
+
+
+@pytest.mark.parametrize("call", ["patch", "sparse_attn"])
+def test_fp16_copy_without_selected_rows(call):
+    """max_rows = 0 (no prompt selects a row): nothing is patched or attended,
+    but a caller-kept fp16 copy of V is still rebuilt from the V cache, and a
+    value fp16 cannot hold still sets the status word; the caches are left
+    alone."""
+    _need_gpu()
+    from paper_2608_21362_amd import kvb
+
+    rng = np.random.default_rng(9)
+    L, hq, hkv, d, T = 2, 8, 2, 64, 200
+    cu = np.array([0, 120, T], np.int32)
+    kc, vc = _bf16(rng, (L, hkv, T, d)), _bf16(rng, (L, hkv, T, d), scale=3.0)
+    vc[1, 1, 150, 7] = numerics.f32_to_bf16_bits(np.array([-1e5], np.float32))[0]
+    dk, dv = (torch.from_numpy(x.view(np.int16)).cuda() for x in (kc, vc))
+    dkf, dvf = (torch.from_numpy(_bf16(rng, (L, hkv, T, d)).view(np.int16)).cuda() for _ in range(2))
+    dq = torch.from_numpy(_bf16(rng, (L, T, hq, d)).view(np.int16)).cuda()
+    rows = torch.full((T,), -1, dtype=torch.int32, device="cuda")
+    cu_rows = torch.zeros(3, dtype=torch.int32, device="cuda")
+    dcu = torch.from_numpy(cu).cuda()
+    v16 = torch.full((L, hkv, T, d), 0x7E00, dtype=torch.int16, device="cuda")
+    status = torch.zeros(4, dtype=torch.int32, device="cuda")
+    if call == "patch":
+        pbytes = kvb.kvb_attn_plans_bytes(L, hq, hkv, d, T, 2, 120, 0)
+        plans = torch.empty(max(pbytes, 16), dtype=torch.uint8, device="cuda")
+        kvb.kvb_patch(L, hq, hkv, d, T, dcu, 2, 120, rows, cu_rows, 0, 0, dkf, dvf, dk, dv, v16,
+                      plans, pbytes, v_status=status)
+    else:
+        out = torch.full((L, T, hq, d), -1, dtype=torch.int16, device="cuda")
+        wsb = kvb.kvb_sparse_attn_workspace_bytes(L, hq, hkv, d, T, 2, 120, 0, 1)
+        ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+        kvb.kvb_sparse_attn(L, hq, hkv, d, T, dcu, 2, 120, rows, cu_rows, 0, 0, dq, dkf, dvf, dk,
+                            dv, v16, 1.0 / np.sqrt(d), kvb.KVB_BF16, out, ws, wsb,
+                            v_status=status)
+        torch.cuda.synchronize()
+        assert np.all(out.cpu().numpy() == -1), "an output row was written"
+    torch.cuda.synchronize()
+    assert np.array_equal(dk.cpu().numpy().view(np.uint16), kc)
+    assert np.array_equal(dv.cpu().numpy().view(np.uint16), vc)
+    assert np.array_equal(v16.cpu().numpy().view(np.uint16), _f16_of_bf16(vc))
+    assert int(status[0].item()) == 1
