@@ -101,6 +101,12 @@ constexpr int kFirstShareNum = 8, kFirstShareDen = 5;
 // is never above the true maximum: a reference above it would push the
 // largest probabilities toward fp16's subnormal range.
 constexpr float kLazy = 15.0f;
+// Reference of a lane that has seen no visible key: finite and far below any
+// scaled score, so that the first visible block always moves the reference
+// (with factor exp2(kNoKey - m) = 0 for the still empty sums), a masked score
+// (-inf) gives probability 0 against it, and no special case is needed for
+// infinities in the block loop.
+constexpr float kNoKey = -1.0e30f;
 
 #define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
 
@@ -249,29 +255,33 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 }
 
 // Issue the asynchronous loads of one 32-key block of K (bf16) and V (fp16)
-// into one LDS stage.  The buffer resources cover exactly the cache rows of
-// this (layer, kv head); rows past the end read as zero (their scores are
-// masked).
+// into one LDS stage.  Each load takes a buffer resource that starts at the
+// block's first row and covers the cache rows of this (layer, kv head) from
+// there on (built on the scalar unit: the lanes add no block offset); rows
+// past the end read as zero (their scores are masked).
 template <int D>
-__device__ __forceinline__ void issue_block(i32x4 krs, i32x4 vrs, int kb, const LoadOffsets<D>& lo,
-                                            char* k_st, char* v_st, int wave) {
+__device__ __forceinline__ void issue_block(const uint16_t* kbase, const uint16_t* vbase, int T,
+                                            int kb, const LoadOffsets<D>& lo, char* k_st,
+                                            char* v_st, int wave) {
   using C = AttnCfg<D>;
-  // the block offset goes into the lane offset: the buffer range check covers
-  // the lane offset, not the scalar one
-  const int boff = kb * C::ROWB;
-  const uint32_t kbase = __builtin_amdgcn_readfirstlane(lds_addr(k_st) + wave * C::LOADS * 1024);
-  const uint32_t vbase = __builtin_amdgcn_readfirstlane(lds_addr(v_st) + wave * C::LOADS * 1024);
+  const int bytes = max(T - kb, 0) * C::ROWB;
+  const i32x4 krs = buffer_rsrc(kbase + (int64_t)kb * D, bytes);
+  const i32x4 vrs = buffer_rsrc(vbase + (int64_t)kb * D, bytes);
+  const uint32_t kl = __builtin_amdgcn_readfirstlane(lds_addr(k_st) + wave * C::LOADS * 1024);
+  const uint32_t vl = __builtin_amdgcn_readfirstlane(lds_addr(v_st) + wave * C::LOADS * 1024);
 #pragma unroll
   for (int i = 0; i < C::LOADS; ++i) {
-    lds_dma16(krs, kbase + i * 1024, boff + lo.k[i], 0);
-    lds_dma16(vrs, vbase + i * 1024, boff + lo.v[i], 0);
+    lds_dma16(krs, kl + i * 1024, lo.k[i], 0);
+    lds_dma16(vrs, vl + i * 1024, lo.v[i], 0);
   }
 }
 
 template <int D>
 struct AttnState {
   f32x16 o[AttnCfg<D>::ND];
-  float m_raw;   // running maximum of raw scores (stale by at most kLazy / scale)
+  float mc;      // reference of the probabilities in log2 units (the running
+                 // maximum of the scaled scores, stale by at most kLazy), or
+                 // kNoKey while this lane has seen no visible key
   float l_part;  // this lane's share of the running sum
 };
 
@@ -367,24 +377,20 @@ __device__ __forceinline__ void softmax_block(f32x16 sacc, AttnState<D>& st, flo
   float bmax = sacc[0];
 #pragma unroll
   for (int r = 1; r < 16; ++r) bmax = fmaxf(bmax, sacc[r]);
-  bmax = max_halves(bmax);
-  const float m_new = fmaxf(st.m_raw, bmax);
-  // a lane with no visible key yet (-inf before and after) does not force a
-  // rescale: its probabilities are 0 against any reference
-  const bool grow = (m_new - st.m_raw) * c_log2 > kLazy ||
-                    (st.m_raw == -INFINITY && m_new != -INFINITY);
-  if (__builtin_expect(__builtin_amdgcn_ballot_w64(grow) != 0, 0)) {
-    const float alpha = (st.m_raw == -INFINITY || m_new == -INFINITY)
-                            ? (m_new == -INFINITY ? 1.0f : 0.0f)
-                            : __builtin_amdgcn_exp2f((st.m_raw - m_new) * c_log2);
+  // the block's maximum in log2 units (-inf for a lane with no visible key in
+  // it: such a lane never forces a rescale)
+  const float bm = max_halves(bmax) * c_log2;
+  if (__builtin_expect(__builtin_amdgcn_ballot_w64(bm - st.mc > kLazy) != 0, 0)) {
+    const float mc_new = fmaxf(st.mc, bm);
+    const float alpha = __builtin_amdgcn_exp2f(st.mc - mc_new);
     st.l_part *= alpha;
 #pragma unroll
     for (int dt = 0; dt < C::ND; ++dt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) st.o[dt][r] *= alpha;
-    st.m_raw = m_new;
+    st.mc = mc_new;
   }
-  const float mc = st.m_raw == -INFINITY ? 0.0f : st.m_raw * c_log2;
+  const float mc = st.mc;
   const f16x2 ones = {(_Float16)1.0f, (_Float16)1.0f};
   float psum = st.l_part;
 #pragma unroll
@@ -447,20 +453,20 @@ __device__ __forceinline__ void attend_segment(
   const int t_min = rws[min(tl.r_begin + wave * rows_per_wave, tl.r_end - 1)];
 
   const int64_t kv_base = ((int64_t)l * Hkv + g) * t_total * D;
-  const i32x4 krs = buffer_rsrc(kc + kv_base, T * C::ROWB);
-  const i32x4 vrs = buffer_rsrc(v16 + kv_base, T * C::ROWB);
+  const uint16_t* const kbase = kc + kv_base;
+  const uint16_t* const vbase = v16 + kv_base;
   const LoadOffsets<D> lo = load_offsets<D>(wave, lane);
   const int nblk = (k_hi - k_lo + kKB - 1) / kKB;
   static_assert(kStages == 5, "stage index arithmetic assumes a 5-deep ring");
 
   // The first four blocks depend only on the tile: they are requested while
   // the query rows are on their way.
-  issue_block<D>(krs, vrs, k_lo, lo, k_ring, v_ring, wave);
-  if (nblk > 1) issue_block<D>(krs, vrs, k_lo + kKB, lo, k_ring + C::BLK, v_ring + C::BLK, wave);
+  issue_block<D>(kbase, vbase, T, k_lo, lo, k_ring, v_ring, wave);
+  if (nblk > 1) issue_block<D>(kbase, vbase, T, k_lo + kKB, lo, k_ring + C::BLK, v_ring + C::BLK, wave);
   if (nblk > 2)
-    issue_block<D>(krs, vrs, k_lo + 2 * kKB, lo, k_ring + 2 * C::BLK, v_ring + 2 * C::BLK, wave);
+    issue_block<D>(kbase, vbase, T, k_lo + 2 * kKB, lo, k_ring + 2 * C::BLK, v_ring + 2 * C::BLK, wave);
   if (nblk > 3)
-    issue_block<D>(krs, vrs, k_lo + 3 * kKB, lo, k_ring + 3 * C::BLK, v_ring + 3 * C::BLK, wave);
+    issue_block<D>(kbase, vbase, T, k_lo + 3 * kKB, lo, k_ring + 3 * C::BLK, v_ring + 3 * C::BLK, wave);
 
   const bool qvalid = t_q >= tl.kstart && t_q < tl.kend;  // rows outside the prompt are skipped
   if (!qvalid) t_q = -1;
@@ -484,7 +490,7 @@ __device__ __forceinline__ void attend_segment(
   AttnState<D> st;
 #pragma unroll
   for (int dt = 0; dt < C::ND; ++dt) st.o[dt] = f32x16{};
-  st.m_raw = -INFINITY;
+  st.mc = kNoKey;
   st.l_part = 0.0f;
 
   // Software pipeline over blocks: step j turns the scores of block j into
@@ -513,7 +519,7 @@ __device__ __forceinline__ void attend_segment(
     __builtin_amdgcn_s_barrier();
     compiler_fence();
     if (j + 4 < nblk)
-      issue_block<D>(krs, vrs, kb + 4 * kKB, lo, k_ring + ((S + 4) % 5) * C::BLK,
+      issue_block<D>(kbase, vbase, T, kb + 4 * kKB, lo, k_ring + ((S + 4) % 5) * C::BLK,
                      v_ring + ((S + 4) % 5) * C::BLK, wave);
     const bool full = (kb + kKB - 1 <= t_min) && (kb + kKB <= k_hi);
     f16x8 pb[2];
@@ -591,7 +597,7 @@ __device__ __forceinline__ void attend_segment(
       float* ml = reinterpret_cast<float*>(reinterpret_cast<char*>(parts) + rec_ml_offset<D>(n_rec)) +
                   ((int64_t)rec * kQT + qi) * 2;
       *reinterpret_cast<float2*>(ml) =
-          make_float2(st.m_raw == -INFINITY ? -INFINITY : st.m_raw * c_log2, l_run);
+          make_float2(st.mc == kNoKey ? -INFINITY : st.mc, l_run);
     }
   }
 }
