@@ -535,8 +535,10 @@ __device__ __forceinline__ void attend_segment(
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_setprio(0);
     // operands of the next step (landed and visible since this step's
-    // barrier; stale past the end of the segment, never used)
+    // barrier; stale past the end of the segment, never used).  K first: LDS
+    // reads return in order and the next step starts with the score products.
     read_k<D>(k_ring + ((S + 2) % 5) * C::BLK, lane, kr);
+    compiler_fence();
     read_v<D>(v_ring + ((S + 1) % 5) * C::BLK, lane, vr);
   };
   using S0 = std::integral_constant<int, 0>;
