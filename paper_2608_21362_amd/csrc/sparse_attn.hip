@@ -89,12 +89,13 @@ constexpr int kSegCost = 7;
 // With two workgroups per CU the dispatcher gives workgroups 0 .. CUs-1 the
 // first slot of every CU and the rest the second; the hardware issues the
 // older (first) workgroup's waves first, so it progresses faster while both
-// run (about 1.2 to 1.4 times per block in timestamped runs).  Balanced ranges
-// give first-slot workgroups 8/5 of the units of second-slot ones so that the
-// two finish together (measured on MI355X at 8K keys per prompt: 8/5 and 3/2
-// gave the shortest launches, 7/5 and 13/10 about 1 % longer; a different
-// placement only costs balance, never correctness).
-constexpr int kFirstShareNum = 8, kFirstShareDen = 5;
+// run (per unit of the plan about 1.5 times as fast in a timestamped per-layer
+// launch at 8K keys per prompt).  Balanced ranges give first-slot workgroups
+// 3/2 of the units of second-slot ones so that the two finish together
+// (measured on MI355X: 3/2 gave the shortest per-layer launches, 8/5 and 7/5
+// 0.3 to 0.9 % longer; a different placement only costs balance, never
+// correctness).
+constexpr int kFirstShareNum = 3, kFirstShareDen = 2;
 // Lazy rescaling: the running maximum (the reference of the probabilities)
 // moves only when a block's maximum exceeds it by more than kLazy log2 units,
 // so probabilities stay below 2^15 (fp16 holds up to 65504).  The reference
