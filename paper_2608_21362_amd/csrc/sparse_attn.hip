@@ -636,8 +636,22 @@ __device__ __forceinline__ int unit_owner(int u, int c1, int c2, int n2) {
 
 // Range index of workgroup w (workgroups 0 .. n_first-1 take the first slot of
 // each CU).
+// Within each slot group, consecutive ranges (which share tiles, and so key
+// blocks) go to workgroups on one XCD: workgroup offset o of a group of g
+// (XCD o % 8 under round-robin dispatch) takes group position (o % 8) g/8 +
+// o / 8 when g is a multiple of 8 (else the identity).
+__device__ __forceinline__ int xcd_pos(int o, int g) {
+  return (g % 8 == 0) ? (o % 8) * (g / 8) + o / 8 : o;
+}
+__device__ __forceinline__ int xcd_off(int i, int g) {
+  return (g % 8 == 0) ? 8 * (i % (g / 8)) + i / (g / 8) : i;
+}
 __device__ __forceinline__ int range_of(int w, int n_first, int n2) {
-  return w >= n_first ? w - n_first : n2 + w;
+  return w >= n_first ? xcd_pos(w - n_first, n2) : n2 + xcd_pos(w, n_first);
+}
+// Workgroup of range index v (inverse of range_of).
+__device__ __forceinline__ int wg_of_range(int v, int n_first, int n2) {
+  return v < n2 ? n_first + xcd_off(v, n2) : xcd_off(v - n2, n_first);
 }
 
 // Work decomposition.  Work unit = one 32-key block of one tile, and a tile
@@ -737,7 +751,7 @@ __device__ __forceinline__ void build_plan(
       const int u = unit_start(v, c1, c2, n2);
       if (u >= p1) break;
       if (u >= p0) {
-        const int w = v < n2 ? v + n_first : v - n2;  // inverse of range_of
+        const int w = wg_of_range(v, n_first, n2);
         seg[2 * w] = make_int4(t, p0, p1, 0);
         seg[2 * w + 1] = mt;
       }
@@ -745,7 +759,7 @@ __device__ __forceinline__ void build_plan(
   }
   for (int v = tid; v < n_wg; v += nt)
     if (unit_start(v, c1, c2, n2) >= total) {
-      const int w = v < n2 ? v + n_first : v - n2;
+      const int w = wg_of_range(v, n_first, n2);
       seg[2 * w] = make_int4(n_tiles, total, total, 0);
       seg[2 * w + 1] = make_int4(0, 0, 0, 0);
     }
