@@ -656,9 +656,11 @@ __device__ __forceinline__ int wg_of_range(int v, int n_first, int n2) {
 
 // Work decomposition.  Work unit = one 32-key block of one tile, and a tile
 // with blocks also counts kSegCost units for its fixed cost (they come first
-// and hold no blocks); units are numbered tile by tile, tiles slot-major (tile
-// index = slot * (layers x kv heads) + layer x kv head: the first row tiles of
-// every prompt, which attend to the fewest keys, come first).  One workgroup
+// and hold no blocks); units are numbered tile by tile, tiles ordered by
+// (layer x kv head) and within it by row slot (tile index = layer x kv head *
+// tile_slots + slot: a (layer, kv head)'s tiles, which share their key blocks,
+// are adjacent, and its first row tiles, which attend to the fewest keys, come
+// first; launches of whole tiles order them slot-major instead).  One workgroup
 // builds the exclusive prefix sum of the tiles' unit counts, then the
 // attention workgroup with range index v takes the contiguous units
 // [unit_start(v), unit_start(v + 1)): c2 units for each of the first n2
@@ -691,8 +693,7 @@ __device__ __forceinline__ void build_plan(
     const int t = base + tid;
     int nb = 0;
     if (t < n_tiles) {
-      const int n_lg = n_tiles / tile_slots;
-      const int lg = t % n_lg, slot = t / n_lg;
+      const int lg = t / tile_slots, slot = t % tile_slots;
       const int64_t set = rows_per_layer ? lg / Hkv : 0;
       const int32_t* cur = cu_rows + set * (n_seqs + 1);
       Tile tile;
@@ -888,7 +889,6 @@ attn_kernel(int32_t balanced, int32_t n_tiles, int32_t Hq, int32_t Hkv, int32_t 
   const int4* sd = reinterpret_cast<const int4*>(plan + range_seg_offset(n_tiles)) + 2 * blockIdx.x;
   const int4 s0 = sd[0];
   int4 mt = sd[1];
-  const int n_lg = n_tiles / tile_slots;
   const int v = range_of(blockIdx.x, (int)gridDim.x - n2, n2);  // range index
   const int32_t* prefix = plan + 4;
   const int4* meta = reinterpret_cast<const int4*>(plan + tile_meta_offset(n_tiles));
@@ -903,7 +903,7 @@ attn_kernel(int32_t balanced, int32_t n_tiles, int32_t Hq, int32_t Hkv, int32_t 
       if (b_hi > b_lo) {
         const int rec = (u <= p0 + kSegCost && p1 <= u_end) ? -1 : 2 * v + (seg == 0 ? 0 : 1);
         SegTile tl;
-        tl.lg = t % n_lg;
+        tl.lg = t / tile_slots;
         tl.r_begin = mt.x;
         tl.r_end = mt.y;
         tl.kstart = mt.z;
@@ -945,7 +945,7 @@ combine_kernel(int32_t n_tiles, int32_t n_wg_max, int32_t Hq, int32_t Hkv, int32
   const int e = blockIdx.y * blockDim.x + threadIdx.x;
   if (e >= kQT * Q8) return;
   const int qi = e / Q8, c8 = (e % Q8) * 8;
-  const int lg = t % (n_tiles / tile_slots);
+  const int lg = t / tile_slots;
   const int l = lg / Hkv, g = lg % Hkv;
   const int wave = qi / kQW, nq = qi % kQW;
   const int row_idx = mt.x + wave * (kQW >> log2g) + (nq >> log2g);
