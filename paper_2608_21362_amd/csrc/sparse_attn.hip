@@ -605,7 +605,7 @@ __device__ __forceinline__ void attend_segment(
   }
 }
 
-// Plan area (int32): [0] c1, [1] c2, [2] n_second, [3] total, [4 .. 4+n_tiles]
+// Plan area (int32): [0] c1, [1] c2, [2] n_first, [3] total, [4 .. 4+n_tiles]
 // prefix, then the per-tile metadata (int4) at tile_meta_offset, then one
 // 32-byte first-segment descriptor per workgroup at range_seg_offset.
 __host__ __device__ constexpr int64_t tile_meta_offset(int64_t n_tiles) {
@@ -618,40 +618,44 @@ __host__ __device__ constexpr int64_t plan_ints(int64_t n_tiles, int64_t n_wg_ma
   return range_seg_offset(n_tiles) + 8 * n_wg_max;
 }
 
-// Ranges are numbered by a range index v: the n2 second-slot workgroups take
-// ranges 0 .. n2-1 (c2 units each), the first-slot ones the ranges after them
-// (c1 units each).  Tiles are ordered shortest first (below), so the tiles
-// with the fewest blocks -- the workgroups that cover several of them pay a
-// segment's fixed cost several times -- go to second-slot workgroups, for which
-// the segment cost in units (kSegCost) is closest to its time.
-__device__ __forceinline__ int unit_start(int v, int c1, int c2, int n2) {
-  return v < n2 ? v * c2 : n2 * c2 + (v - n2) * c1;
+// Ranges are numbered by a range index v in unit order.  With two workgroups
+// per CU (n_first > 0: workgroups 0 .. n_first-1 take the first slot of every
+// CU, the other n_first the second), range 2p belongs to the second-slot
+// workgroup of CU position p and range 2p + 1 to its first-slot partner, so a
+// CU's two workgroups cover adjacent units (the same tiles, and so the same key
+// blocks); second-slot ranges hold c2 units, first-slot ones c1.  With one
+// workgroup per CU (n_first == 0) range v holds c2 units.  CU positions are
+// grouped by XCD: workgroup offset o of a group of g (XCD o % 8 under
+// round-robin dispatch) takes position (o % 8) g/8 + o / 8 when g is a multiple
+// of 8 (else the identity), so consecutive ranges share an XCD and its L2.
+__device__ __forceinline__ int unit_start(int v, int c1, int c2, int n_first) {
+  return n_first > 0 ? (v / 2) * (c1 + c2) + (v % 2) * c2 : v * c2;
 }
 
 // Range index whose units hold unit u.
-__device__ __forceinline__ int unit_owner(int u, int c1, int c2, int n2) {
-  const int b = n2 * c2;
-  return u < b ? u / c2 : n2 + (u - b) / c1;
+__device__ __forceinline__ int unit_owner(int u, int c1, int c2, int n_first) {
+  if (n_first == 0) return u / c2;
+  const int j = u / (c1 + c2);
+  return 2 * j + (u - j * (c1 + c2) >= c2 ? 1 : 0);
 }
 
-// Range index of workgroup w (workgroups 0 .. n_first-1 take the first slot of
-// each CU).
-// Within each slot group, consecutive ranges (which share tiles, and so key
-// blocks) go to workgroups on one XCD: workgroup offset o of a group of g
-// (XCD o % 8 under round-robin dispatch) takes group position (o % 8) g/8 +
-// o / 8 when g is a multiple of 8 (else the identity).
 __device__ __forceinline__ int xcd_pos(int o, int g) {
   return (g % 8 == 0) ? (o % 8) * (g / 8) + o / 8 : o;
 }
 __device__ __forceinline__ int xcd_off(int i, int g) {
   return (g % 8 == 0) ? 8 * (i % (g / 8)) + i / (g / 8) : i;
 }
-__device__ __forceinline__ int range_of(int w, int n_first, int n2) {
-  return w >= n_first ? xcd_pos(w - n_first, n2) : n2 + xcd_pos(w, n_first);
+
+// Range index of workgroup w of n_wg (n_wg = 2 n_first when n_first > 0).
+__device__ __forceinline__ int range_of(int w, int n_first, int n_wg) {
+  if (n_first == 0) return xcd_pos(w, n_wg);
+  return w >= n_first ? 2 * xcd_pos(w - n_first, n_first) : 2 * xcd_pos(w, n_first) + 1;
 }
+
 // Workgroup of range index v (inverse of range_of).
-__device__ __forceinline__ int wg_of_range(int v, int n_first, int n2) {
-  return v < n2 ? n_first + xcd_off(v, n2) : xcd_off(v - n2, n_first);
+__device__ __forceinline__ int wg_of_range(int v, int n_first, int n_wg) {
+  if (n_first == 0) return xcd_off(v, n_wg);
+  return (v % 2 == 0) ? n_first + xcd_off(v / 2, n_first) : xcd_off(v / 2, n_first);
 }
 
 // Work decomposition.  Work unit = one 32-key block of one tile, and a tile
@@ -663,9 +667,9 @@ __device__ __forceinline__ int wg_of_range(int v, int n_first, int n2) {
 // first; launches of whole tiles order them slot-major instead).  One workgroup
 // builds the exclusive prefix sum of the tiles' unit counts, then the
 // attention workgroup with range index v takes the contiguous units
-// [unit_start(v), unit_start(v + 1)): c2 units for each of the first n2
-// ranges (second-slot workgroups), c1 for the others, sized to cover every unit.
-//   plan[0] = c1, plan[1] = c2, plan[2] = n2, plan[3] = total,
+// [unit_start(v), unit_start(v + 1)): c2 units for second-slot workgroups,
+// c1 for first-slot ones (above), sized to cover every unit.
+//   plan[0] = c1, plan[1] = c2, plan[2] = n_first, plan[3] = total,
 //   plan[4 .. 4+n_tiles] = prefix,
 //   per tile an int4 {first row entry, end row entry, key start, key end} at
 //   the 16-byte aligned offset tile_meta_offset(n_tiles),
@@ -730,11 +734,10 @@ __device__ __forceinline__ void build_plan(
   const int64_t weight = (int64_t)kFirstShareNum * n_first + (int64_t)kFirstShareDen * (n_wg - n_first);
   const int c2 = (int)max((int64_t)1, ((int64_t)kFirstShareDen * total + weight - 1) / weight);
   const int c1 = (int)(((int64_t)kFirstShareNum * c2 + kFirstShareDen - 1) / kFirstShareDen);
-  const int n2 = n_wg - n_first;
   if (tid == 0) {
     plan[0] = c1;
     plan[1] = c2;
-    plan[2] = n2;
+    plan[2] = n_first;
     plan[3] = total;
     prefix[n_tiles] = total;
     prefix_sh[n_tiles] = total;
@@ -748,19 +751,19 @@ __device__ __forceinline__ void build_plan(
     const int p0 = prefix_sh[t], p1 = prefix_sh[t + 1];
     if (p1 <= p0) continue;
     const int4 mt = meta[t];
-    for (int v = unit_owner(p0, c1, c2, n2); v < n_wg; ++v) {
-      const int u = unit_start(v, c1, c2, n2);
+    for (int v = unit_owner(p0, c1, c2, n_first); v < n_wg; ++v) {
+      const int u = unit_start(v, c1, c2, n_first);
       if (u >= p1) break;
       if (u >= p0) {
-        const int w = wg_of_range(v, n_first, n2);
+        const int w = wg_of_range(v, n_first, n_wg);
         seg[2 * w] = make_int4(t, p0, p1, 0);
         seg[2 * w + 1] = mt;
       }
     }
   }
   for (int v = tid; v < n_wg; v += nt)
-    if (unit_start(v, c1, c2, n2) >= total) {
-      const int w = wg_of_range(v, n_first, n2);
+    if (unit_start(v, c1, c2, n_first) >= total) {
+      const int w = wg_of_range(v, n_first, n_wg);
       seg[2 * w] = make_int4(n_tiles, total, total, 0);
       seg[2 * w + 1] = make_int4(0, 0, 0, 0);
     }
@@ -885,15 +888,15 @@ attn_kernel(int32_t balanced, int32_t n_tiles, int32_t Hq, int32_t Hkv, int32_t 
   }
   // the plan's head and this workgroup's first-segment descriptor are
   // independent loads: the first tile's blocks can be requested right after
-  const int c1 = plan[0], c2 = plan[1], n2 = plan[2], total = plan[3];
+  const int c1 = plan[0], c2 = plan[1], n_first = plan[2], total = plan[3];
   const int4* sd = reinterpret_cast<const int4*>(plan + range_seg_offset(n_tiles)) + 2 * blockIdx.x;
   const int4 s0 = sd[0];
   int4 mt = sd[1];
-  const int v = range_of(blockIdx.x, (int)gridDim.x - n2, n2);  // range index
+  const int v = range_of(blockIdx.x, n_first, (int)gridDim.x);  // range index
   const int32_t* prefix = plan + 4;
   const int4* meta = reinterpret_cast<const int4*>(plan + tile_meta_offset(n_tiles));
-  int u = unit_start(v, c1, c2, n2);
-  const int u_end = min(unit_start(v + 1, c1, c2, n2), total);
+  int u = unit_start(v, c1, c2, n_first);
+  const int u_end = min(unit_start(v + 1, c1, c2, n_first), total);
   int t = s0.x, p0 = s0.y, p1 = s0.z;
   for (int seg = 0; u < u_end && t < n_tiles;) {
     if (p1 > u) {  // else an empty tile
@@ -934,12 +937,13 @@ combine_kernel(int32_t n_tiles, int32_t n_wg_max, int32_t Hq, int32_t Hkv, int32
                int32_t tile_slots, const int32_t* __restrict__ plan, int32_t n_rec,
                int32_t out_f32, void* __restrict__ out, const float* __restrict__ parts) {
   const int t = blockIdx.x;
-  const int c1 = plan[0], c2 = plan[1], n2 = plan[2];
+  const int c1 = plan[0], c2 = plan[1], n_first = plan[2];
   const int p0 = plan[4 + t], p1 = plan[5 + t];
   const int4 mt = reinterpret_cast<const int4*>(plan + tile_meta_offset(n_tiles))[t];
   if (p1 <= p0) return;
   // the tile's blocks are units [p0 + kSegCost, p1), held by ranges w_a .. w_b
-  const int w_a = unit_owner(p0 + kSegCost, c1, c2, n2), w_b = unit_owner(p1 - 1, c1, c2, n2);
+  const int w_a = unit_owner(p0 + kSegCost, c1, c2, n_first),
+            w_b = unit_owner(p1 - 1, c1, c2, n_first);
   if (w_a == w_b) return;  // finished by one workgroup
   constexpr int Q8 = D / 8;  // 8-channel pieces per query vector
   const int e = blockIdx.y * blockDim.x + threadIdx.x;
@@ -955,7 +959,7 @@ combine_kernel(int32_t n_tiles, int32_t n_wg_max, int32_t Hq, int32_t Hkv, int32
   // the tile is the first segment of every range after w_a, and of w_a only
   // if w_a's range starts inside the tile (a range that starts before it ends
   // with blocks of an earlier tile)
-  const int rec_a = 2 * w_a + (unit_start(w_a, c1, c2, n2) < p0 ? 1 : 0);
+  const int rec_a = 2 * w_a + (unit_start(w_a, c1, c2, n_first) < p0 ? 1 : 0);
   const int n_parts = w_b - w_a + 1;
   const uint16_t* o16 = reinterpret_cast<const uint16_t*>(parts);
   const float* ml = reinterpret_cast<const float*>(reinterpret_cast<const char*>(parts) +
