@@ -83,9 +83,10 @@ constexpr int kAttnMaxWorkgroups = 1024;  // attention workgroups (sizes the par
 // segment's start (tile rows, queries and the first blocks fetched) and end
 // (output or partial record written), so that workgroups covering many short
 // tiles get fewer blocks.  Measured on MI355X at 8K keys per prompt: a
-// segment's start and end take as long as five to eight blocks, and 7 gave
-// the shortest per-layer launches of the values tried (0, 2, 4, 7).
-constexpr int kSegCost = 7;
+// segment's start and end take as long as five to eight blocks; with a CU's
+// two workgroups on adjacent ranges, 11 gave the shortest per-layer launches
+// of the values tried (7, 9, 11, 13).
+constexpr int kSegCost = 11;
 // With two workgroups per CU the dispatcher gives workgroups 0 .. CUs-1 the
 // first slot of every CU and the rest the second; the hardware issues the
 // older (first) workgroup's waves first, so it progresses faster while both
