@@ -12,6 +12,11 @@
 // Gv % 8 == 0; the API asks Gv % 16), so 16 (d = 128) or 8 (d = 64) lanes
 // store a whole row and a wave's stores are contiguous.  Every value input of
 // the thread is loaded before the key work starts, so those loads overlap it.
+// The fused kernel (below) instead stages each head's key statistics and the
+// rotation row in LDS and reads them for every token, and loads its value
+// inputs after the key work: neither is then held in registers while a key
+// job's loads are in flight (158 instead of 231 registers, three waves per
+// SIMD instead of two).
 //
 // Arithmetic is double with contraction off: x = fma(code, scale, zero) is
 // exact in the product (8-bit code times 24-bit scale), so it equals the
@@ -68,35 +73,62 @@ stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
   const int ngk = kC / Gk, ngv = D / Gv;
   // fused deviation: running cosine sum over heads of this thread's four tokens
   double cos_sum[4] = {0.0, 0.0, 0.0, 0.0};
+  // fused: the head's key statistics (scale, then zero; at most C/4 groups)
+  // and the chunk's rotation row (cos, then sin) staged in LDS, read per token
+  __shared__ float4 st_k4[DEV ? 2 * (kC / 4) * D / 4 : 1];
+  __shared__ float4 st_r4[DEV ? D / 4 : 1];
   const int n_heads = DEV ? Hkv : 1;
   for (int hh = 0; hh < n_heads; ++hh) {
     const int l = DEV ? (int)blockIdx.y : (int)blockIdx.y / Hkv;
     const int h = DEV ? hh : (int)blockIdx.y % Hkv;
     const int64_t slab = ((int64_t)ch.pool_idx * L + l) * Hkv + h;  // (p, l, h)
     const int64_t out_row0 = ((int64_t)l * Hkv + h) * t_total + ch.dst_row;
+    if constexpr (DEV) {
+      // the previous head's key jobs are done with the staged statistics
+      __syncthreads();
+      const int n4 = ngk * D / 4;
+      const float4* ks4 = reinterpret_cast<const float4*>(k_scale + slab * ngk * D);
+      const float4* kz4 = reinterpret_cast<const float4*>(k_zero + slab * ngk * D);
+      for (int i = threadIdx.x; i < n4; i += blockDim.x) {
+        st_k4[i] = ks4[i];
+        st_k4[n4 + i] = kz4[i];
+      }
+      if (threadIdx.x < H / 4) {
+        st_r4[threadIdx.x] = reinterpret_cast<const float4*>(rope_cos + (int64_t)c * H)[threadIdx.x];
+        st_r4[H / 4 + threadIdx.x] =
+            reinterpret_cast<const float4*>(rope_sin + (int64_t)c * H)[threadIdx.x];
+      }
+      __syncthreads();
+    }
 
-    // value inputs of this thread's pieces (token u, channels [j0, j0 + 8))
+    // value inputs of this thread's pieces (token u, channels [j0, j0 + 8));
+    // the plain stitch requests them before its key work (they are in flight
+    // while the keys are computed), the fused one after it (fewer live
+    // registers during the key jobs)
     constexpr int VP = D / 8;              // pieces per token row
     constexpr int VPT = kC * VP / 256;     // pieces per thread
     uint32_t vw[VPT][2];
     float vsc[VPT], vzr[VPT];
+    auto load_values = [&]() {
 #pragma unroll
-    for (int k = 0; k < VPT; ++k) {
-      const int vj = threadIdx.x + 256 * k;
-      const int u = vj / VP, j0 = (vj % VP) * 8;
-      const int64_t srow = slab * kC + u;
-      vsc[k] = v_scale[srow * ngv + j0 / Gv];
-      vzr[k] = v_zero[srow * ngv + j0 / Gv];
-      const uint8_t* row = v_codes + srow * CB;
-      if constexpr (BITS == 8) {
-        const uint2 a = *reinterpret_cast<const uint2*>(row + j0);
-        vw[k][0] = a.x;
-        vw[k][1] = a.y;
-      } else {
-        vw[k][0] = *reinterpret_cast<const uint32_t*>(row + j0 / 2);
-        vw[k][1] = 0;
+      for (int k = 0; k < VPT; ++k) {
+        const int vj = threadIdx.x + 256 * k;
+        const int u = vj / VP, j0 = (vj % VP) * 8;
+        const int64_t srow = slab * kC + u;
+        vsc[k] = v_scale[srow * ngv + j0 / Gv];
+        vzr[k] = v_zero[srow * ngv + j0 / Gv];
+        const uint8_t* row = v_codes + srow * CB;
+        if constexpr (BITS == 8) {
+          const uint2 a = *reinterpret_cast<const uint2*>(row + j0);
+          vw[k][0] = a.x;
+          vw[k][1] = a.y;
+        } else {
+          vw[k][0] = *reinterpret_cast<const uint32_t*>(row + j0 / 2);
+          vw[k][1] = 0;
+        }
       }
-    }
+    };
+    if constexpr (!DEV) load_values();
 
     for (int job = threadIdx.x; job < KJOBS; job += blockDim.x) {
       {
@@ -104,25 +136,35 @@ stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
         const int q = job / TPT, cg = job % TPT;
         const int u0 = 4 * q, j0 = 8 * cg;
         const int g = u0 / Gk;
-        const float* sc = k_scale + (slab * ngk + g) * D;
-        const float* zr = k_zero + (slab * ngk + g) * D;
-        // kept as float (half the registers of double) and widened exactly at use
+        // statistics and rotation row of the job's channels, kept as float
+        // (half the registers of double) and widened exactly at use: loaded
+        // once per job for the plain stitch, read from LDS for every token in
+        // the fused kernel (so they are not live while its loads are in flight)
         float s_lo[8], s_hi[8], z_lo[8], z_hi[8], cs[8], sn[8];
+        auto load_stats = [&]() {
+          const float* sc = DEV ? reinterpret_cast<const float*>(st_k4) + g * D
+                                : k_scale + (slab * ngk + g) * D;
+          const float* zr = DEV ? reinterpret_cast<const float*>(st_k4) + (ngk + g) * D
+                                : k_zero + (slab * ngk + g) * D;
+          const float* rc = DEV ? reinterpret_cast<const float*>(st_r4) : rope_cos + (int64_t)c * H;
+          const float* rs = DEV ? reinterpret_cast<const float*>(st_r4) + H : rope_sin + (int64_t)c * H;
 #pragma unroll
-        for (int k = 0; k < 8; k += 4) {
-          const float4 a = *reinterpret_cast<const float4*>(sc + j0 + k);
-          const float4 b = *reinterpret_cast<const float4*>(sc + H + j0 + k);
-          const float4 e = *reinterpret_cast<const float4*>(zr + j0 + k);
-          const float4 f = *reinterpret_cast<const float4*>(zr + H + j0 + k);
-          const float4 cc = *reinterpret_cast<const float4*>(rope_cos + (int64_t)c * H + j0 + k);
-          const float4 ss = *reinterpret_cast<const float4*>(rope_sin + (int64_t)c * H + j0 + k);
-          s_lo[k] = a.x; s_lo[k + 1] = a.y; s_lo[k + 2] = a.z; s_lo[k + 3] = a.w;
-          s_hi[k] = b.x; s_hi[k + 1] = b.y; s_hi[k + 2] = b.z; s_hi[k + 3] = b.w;
-          z_lo[k] = e.x; z_lo[k + 1] = e.y; z_lo[k + 2] = e.z; z_lo[k + 3] = e.w;
-          z_hi[k] = f.x; z_hi[k + 1] = f.y; z_hi[k + 2] = f.z; z_hi[k + 3] = f.w;
-          cs[k] = cc.x; cs[k + 1] = cc.y; cs[k + 2] = cc.z; cs[k + 3] = cc.w;
-          sn[k] = ss.x; sn[k + 1] = ss.y; sn[k + 2] = ss.z; sn[k + 3] = ss.w;
-        }
+          for (int k = 0; k < 8; k += 4) {
+            const float4 a = *reinterpret_cast<const float4*>(sc + j0 + k);
+            const float4 b = *reinterpret_cast<const float4*>(sc + H + j0 + k);
+            const float4 e = *reinterpret_cast<const float4*>(zr + j0 + k);
+            const float4 f = *reinterpret_cast<const float4*>(zr + H + j0 + k);
+            const float4 cc = *reinterpret_cast<const float4*>(rc + j0 + k);
+            const float4 ss = *reinterpret_cast<const float4*>(rs + j0 + k);
+            s_lo[k] = a.x; s_lo[k + 1] = a.y; s_lo[k + 2] = a.z; s_lo[k + 3] = a.w;
+            s_hi[k] = b.x; s_hi[k + 1] = b.y; s_hi[k + 2] = b.z; s_hi[k + 3] = b.w;
+            z_lo[k] = e.x; z_lo[k + 1] = e.y; z_lo[k + 2] = e.z; z_lo[k + 3] = e.w;
+            z_hi[k] = f.x; z_hi[k + 1] = f.y; z_hi[k + 2] = f.z; z_hi[k + 3] = f.w;
+            cs[k] = cc.x; cs[k + 1] = cc.y; cs[k + 2] = cc.z; cs[k + 3] = cc.w;
+            sn[k] = ss.x; sn[k + 1] = ss.y; sn[k + 2] = ss.z; sn[k + 3] = ss.w;
+          }
+        };
+        if constexpr (!DEV) load_stats();
         // the codes of the four tokens (and, fused, their fresh key pieces)
         // are all requested before any is used: one memory round trip per job
         uint32_t cwl[4][2], cwh[4][2];
@@ -148,6 +190,10 @@ stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int u = u0 + i;
+          if constexpr (DEV) {
+            asm volatile("" ::: "memory");  // re-read the staged values for every token
+            load_stats();
+          }
           const uint32_t wl[2] = {cwl[i][0], cwl[i][1]}, wh[2] = {cwh[i][0], cwh[i][1]};
           float ylo[8], yhi[8];
 #pragma unroll
@@ -206,6 +252,7 @@ stitch_kernel(int32_t L, int32_t Hkv, int32_t Gk, int32_t Gv, int32_t n_pool,
     }
 
     // ---- values
+    if constexpr (DEV) load_values();
 #pragma unroll
     for (int k = 0; k < VPT; ++k) {
       const int vj = threadIdx.x + 256 * k;
