@@ -37,6 +37,10 @@ CASES = {
     # token quad are not 16-byte aligned)
     "sink1_3p": kw.scaled(kw.WORKLOADS["long_32k"], n_layers=2, n_prompts=3, chunks_per_prompt=5,
                           n_sinks=1),
+    # the smallest key-statistic group the API takes (4 tokens): 32 groups of
+    # scales and zeros per head, the largest set the fused kernel stages
+    "kgroup4_2l": kw.scaled(kw.WORKLOADS["qwen_36l_8k"], n_layers=2, chunks_per_prompt=5,
+                            k_group=4),
     # nothing cached: the fused call is a no-op (no row is written)
     "cold_2l": kw.scaled(kw.WORKLOADS["qwen_36l_8k"], n_layers=2, chunks_per_prompt=3,
                          placement="prefix_hits", hit_chunks=0, seam_left=16, seam_right=16),
